@@ -1,0 +1,237 @@
+/*
+ * bmlp.h — C ABI of the MI355X train-step library for fully binary multi-layer
+ * perceptrons trained with random local binary error signals (Colombo,
+ * Pittorino, Roveri, arXiv 2412.00119).
+ *
+ * One call of bmlp_train_step is one mini-batch of the paper's Algorithm 1:
+ * for every layer l the bit-packed XNOR-popcount forward z = a W^T and
+ * a = sign(z), the fixed random local classifier y_hat = a P^T, the 01-loss
+ * (Eq. 1) with the robustness margin that selects the patterns to update
+ * (Section 3.2), the choice of the "easiest" wrong perceptron in each group of
+ * gamma (Algorithm 2, Section 3.3), and the Clipped-Perceptron increments plus
+ * stochastic reinforcement of the bounded integer hidden weights, re-binarised
+ * by sign into the visible weights (Algorithm 3, Section 3.4).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Pointers named d_* are DEVICE pointers, h_* are HOST pointers.
+ *  - `stream` is a hipStream_t (NULL = the legacy default stream).  Every call
+ *    that takes a stream only enqueues work on it and returns without
+ *    synchronising; results are visible after the stream is synchronised.
+ *  - The library never allocates or frees device memory.  The caller owns the
+ *    state and workspace buffers (sizes from bmlp_state_bytes and
+ *    bmlp_workspace_bytes, 256-byte aligned) and every input/output buffer, and
+ *    keeps them alive while a context uses them.
+ *  - Bit rows: a row of K values in {-1,+1} is ceil(K/64) little-endian uint64
+ *    words; value j is bit (j % 64) of word (j / 64), bit 1 means +1, and the
+ *    bits past K in the last word are 0.  A uint32 view of the same memory is
+ *    the same layout with 32-bit words.
+ *  - Labels are int32 in [0, n_classes) (the paper numbers classes 1..c).
+ *    A label outside that range is a precondition violation; the result is
+ *    unspecified but stays within the buffers.
+ *  - Return value: BMLP_OK or a negative status.  Argument, shape and
+ *    configuration errors are detected on the host before anything is
+ *    enqueued and leave every buffer untouched.  BMLP_EHIP reports a failed
+ *    kernel launch; bmlp_last_error() then gives the HIP message.  Faults
+ *    inside a kernel surface at the caller's next stream synchronisation.
+ *  - One context is used from one host thread and one stream at a time.
+ */
+#ifndef BMLP_H_
+#define BMLP_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  BMLP_OK = 0,
+  BMLP_EINVAL = -1,   /* bad argument: null pointer, unknown option          */
+  BMLP_ESHAPE = -2,   /* size out of range: n > max_batch, widths, gamma      */
+  BMLP_EHIP = -3,     /* a HIP call or kernel launch failed                   */
+  BMLP_ESTATE = -4,   /* misaligned state/workspace buffer                    */
+};
+
+/* Forward GEMM implementation (the binary contraction z = a W^T). */
+enum {
+  BMLP_FWD_AUTO = 0,      /* the library's fastest implementation              */
+  BMLP_FWD_POPCOUNT = 1,  /* XNOR-popcount over 32-bit words (v_xor + v_bcnt)  */
+};
+
+/* Limits of this build. */
+#define BMLP_MAX_LAYERS 64
+#define BMLP_MAX_WIDTH 32767      /* |z| <= K_{l-1} must fit in int16          */
+#define BMLP_MAX_CLASSES 32767
+#define BMLP_MAX_GROUP 4096       /* gamma, bounded by on-chip bucket storage  */
+#define BMLP_MAX_BATCH 16384      /* pattern indices are kept in 15 bits on chip */
+
+/*
+ * Network and hyper-parameters (Algorithm 1's variables and hyper-parameters;
+ * Section 3.1 for the architecture).
+ *   n_layers     L >= 1 hidden layers (1..BMLP_MAX_LAYERS).
+ *   h_widths     host array of L+1 widths K_0..K_L, each 1..BMLP_MAX_WIDTH; K_0
+ *                is the input width.  Copied by bmlp_init/bmlp_attach.
+ *   n_classes    c, 2..BMLP_MAX_CLASSES.
+ *   max_batch    largest n accepted by the batch calls, 1..BMLP_MAX_BATCH.
+ *   bound        B: hidden weights live in [-B, B].  Odd, 1..127 (8-bit hidden
+ *                weights, Table 4); B = 1 keeps only the visible weights.
+ *   group_size   gamma; must divide every K_l (l >= 1) and be <= BMLP_MAX_GROUP.
+ *                0 selects the paper's rule gamma* per layer (Section 4.3): the
+ *                divisor of K_l closest to [75, 105], ties to the larger.
+ *   robustness   r >= 0 (Section 3.2; the paper uses 0.25, Appendix A.1).  A
+ *                pattern is updated when tau < ceil(r * K_l).
+ *   seed         64-bit key of the Philox4x32-10 streams (init, reinforcement).
+ *   fwd_impl     BMLP_FWD_* .
+ */
+typedef struct bmlp_config {
+  int32_t n_layers;
+  const int32_t *h_widths;
+  int32_t n_classes;
+  int32_t max_batch;
+  int32_t bound;
+  int32_t group_size;
+  double robustness;
+  uint64_t seed;
+  int32_t fwd_impl;
+  int32_t reserved;
+} bmlp_config;
+
+/*
+ * Derived per-layer plan (host-only query; no device work).
+ *   k_in, k_out      K_{l-1}, K_l.
+ *   gamma, groups    group size and G_l = K_l / gamma.
+ *   words_in/out     uint64 words per bit row of a_{l-1} / a_l.
+ *   ld_h             bytes per row of H_l (>= k_in, a multiple of 64).
+ *   robust_thr       ceil(r * K_l), computed in IEEE double.
+ *   off_h, off_w, off_p  byte offsets in the state buffer of
+ *                    H_l  int8   [k_out][ld_h]       hidden weights, perceptron-major
+ *                                                    (the transpose of the paper's
+ *                                                    K_{l-1} x K_l, so h^k is a row);
+ *                                                    bytes past k_in in a row are 0;
+ *                    W_l  uint64 [k_out][words_in]   visible weights sign(H_l), bits;
+ *                    P_l  uint64 [n_classes][words_out]  fixed classifier, row y is rho^y.
+ *   off_a, off_err, off_upd, off_kstar  byte offsets in the workspace of the
+ *                    last train step's
+ *                    a_l    uint64 [max_batch][words_out]
+ *                    err_l  uint8  [max_batch]   01-loss
+ *                    upd_l  uint8  [max_batch]   1 = pattern in M_l
+ *                    kstar_l int16 [max_batch][groups]  easiest wrong
+ *                           perceptron of each group as an offset in the
+ *                           group; -1 when the group has none or the pattern
+ *                           is not in M_l (the pairs of U_l, Algorithm 2).
+ */
+typedef struct bmlp_layer_info {
+  int32_t k_in, k_out, gamma, groups;
+  int32_t words_in, words_out, ld_h, robust_thr;
+  uint64_t off_h, off_w, off_p;
+  uint64_t off_a, off_err, off_upd, off_kstar;
+} bmlp_layer_info;
+
+typedef struct bmlp_ctx bmlp_ctx;   /* opaque, host memory only */
+
+/* Bytes of the state buffer (H, W, P of every layer), or 0 for an invalid
+ * configuration.  A checkpoint is this buffer (or just H and P, see
+ * bmlp_attach) plus the step counter, p_r, the seed and the configuration. */
+size_t bmlp_state_bytes(const bmlp_config *cfg);
+
+/* Bytes of the workspace buffer, or 0 for an invalid configuration. */
+size_t bmlp_workspace_bytes(const bmlp_config *cfg);
+
+/* Validates cfg and fills info for layer l (1..L).  Host only. */
+int bmlp_describe(const bmlp_config *cfg, int32_t l, bmlp_layer_info *info);
+
+/* The reinforcement threshold T_l = ceil(q * 2^32), q = p_r sqrt(2 / (pi K_l))
+ * (Algorithm 3), computed in IEEE double in that order and clamped to
+ * [0, 2^32].  A hidden weight is reinforced when its 32-bit draw is < T_l.
+ * Host only. */
+uint64_t bmlp_reinforce_threshold(double p_r, int32_t k_l);
+
+/* Creates a context over caller-owned buffers and initialises the state:
+ * H_l and P_l uniform on {-1,+1} from Philox streams 1 and 2 (Algorithm 1,
+ * initialisation), W_l = sign(H_l).  d_state and d_workspace must be
+ * 256-byte aligned and of the sizes above.  On success *out receives the
+ * context (free it with bmlp_destroy). */
+int bmlp_init(const bmlp_config *cfg, void *d_state, void *d_workspace, void *stream,
+              bmlp_ctx **out);
+
+/* Like bmlp_init but keeps H_l and P_l already in d_state (a restored
+ * checkpoint) and only recomputes W_l = sign(H_l) from them. */
+int bmlp_attach(const bmlp_config *cfg, void *d_state, void *d_workspace, void *stream,
+                bmlp_ctx **out);
+
+/* Packs an int8 matrix [n][K] of {-1,+1} (any value > 0 counts as +1) into bit
+ * rows [n][ceil(K/64)] (the step before the forward, Algorithm 1: the input
+ * is already binarised).  n >= 0, K >= 1. */
+int bmlp_pack(const int8_t *d_pm1, int32_t n, int32_t K, uint64_t *d_bits, void *stream);
+
+/* Inference (Algorithm 1 forward and local outputs only): writes the local
+ * output y_hat_l of every layer to d_yhat, int32 [L][n][n_classes].
+ * d_x: bit rows [n][words(K_0)].  0 <= n <= max_batch. */
+int bmlp_forward(bmlp_ctx *ctx, const uint64_t *d_x, int32_t n, int32_t *d_yhat, void *stream);
+
+/* One training step on a mini-batch (Algorithm 1 body with Algorithms 2-3).
+ *   d_x      bit rows [n][words(K_0)], d_y int32 [n].
+ *   step     the global step counter t; keys the reinforcement draws, so a run
+ *            restored from a checkpoint continues bit-exactly.
+ *   p_r      reinforcement probability of this step (the epoch rescale
+ *            p_r <- p_r sqrt(E^e) stays with the caller).
+ *   d_stats  int32 [L][4], overwritten with per-layer counts: sum of the
+ *            01-loss, |M_l|, |U_l| (selected pairs), and reinforcement draws
+ *            that fired (0 when M_l is empty, as the layer is then untouched).
+ * Every layer's forward uses the weights from before the step. */
+int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int32_t n,
+                    uint64_t step, double p_r, int32_t *d_stats, void *stream);
+
+/* Evaluation: adds to d_correct[l-1] the number of patterns whose layer-l
+ * local classifier predicts the label (the last layer's classifier is the
+ * network output; earlier ones are early exits, Section 3.1).  The caller
+ * zeroes d_correct (int32 [L]) before the first batch. */
+int bmlp_eval(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int32_t n,
+              int32_t *d_correct, void *stream);
+
+/* Device pointers to H_l, W_l and P_l of layer l (1..L) in the state. */
+int bmlp_layer_views(bmlp_ctx *ctx, int32_t l, int8_t **d_h, uint64_t **d_w, uint64_t **d_p);
+
+/* Device pointers to the last train step's per-layer trace in the workspace
+ * (layouts in bmlp_layer_info). */
+int bmlp_step_trace(bmlp_ctx *ctx, int32_t l, const uint64_t **d_a, const uint8_t **d_err,
+                    const uint8_t **d_upd, const int16_t **d_kstar);
+
+/* Static description of a status code. */
+const char *bmlp_status_string(int status);
+
+/* Message of the last BMLP_EHIP on this thread ("" if none). */
+const char *bmlp_last_error(void);
+
+/* Kernel classes timed by the profiling aid below. */
+enum {
+  BMLP_KERNEL_FWD = 0,      /* hidden-layer forward contraction (z, a)       */
+  BMLP_KERNEL_CLS = 1,      /* local classifier contraction (y_hat)          */
+  BMLP_KERNEL_SELECT = 2,   /* 01-loss, margin, M_l, easiest perceptrons     */
+  BMLP_KERNEL_UPDATE = 3,   /* CP increments, reinforcement, re-sign         */
+  BMLP_KERNEL_OTHER = 4,    /* fills and the rest                            */
+  BMLP_KERNEL_KINDS = 5
+};
+
+/* Profiling aid: brackets each of the next (at most max_launches) kernel
+ * launches of this context with a pair of HIP events on the launch's
+ * stream.  The events are host-created objects; no device buffer is
+ * allocated.  Returns BMLP_EHIP if the events cannot be created. */
+int bmlp_profile_start(bmlp_ctx *ctx, int32_t max_launches);
+
+/* Ends profiling: waits for the last recorded event, then writes per kernel
+ * class the summed duration in milliseconds (h_ms[BMLP_KERNEL_KINDS]) and the
+ * number of timed launches (h_launches[BMLP_KERNEL_KINDS]), and releases the
+ * events.  Either output may be NULL. */
+int bmlp_profile_stop(bmlp_ctx *ctx, double *h_ms, int64_t *h_launches);
+
+/* Frees the host-side context.  Device buffers stay with the caller. */
+void bmlp_destroy(bmlp_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BMLP_H_ */

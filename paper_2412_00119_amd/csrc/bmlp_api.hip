@@ -1,0 +1,456 @@
+// C ABI of the train-step library: validation, state/workspace layout and the
+// launch sequence of Algorithm 1 on the caller's stream.
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "bmlp_internal.h"
+
+struct ProfRec {
+  int kind;
+  hipEvent_t t0, t1;
+};
+
+struct bmlp_ctx {
+  bmlp::Plan plan;
+  uint8_t *state;
+  uint8_t *ws;
+  bool prof_on = false;
+  size_t prof_used = 0;
+  std::vector<ProfRec> prof;
+};
+
+namespace bmlp {
+namespace {
+
+thread_local char g_last_error[256] = "";
+
+int hip_fail(hipError_t e, const char *where) {
+  snprintf(g_last_error, sizeof(g_last_error), "%s: %s", where, hipGetErrorString(e));
+  return BMLP_EHIP;
+}
+
+#define BMLP_LAUNCH(call)                                    \
+  do {                                                       \
+    hipError_t e_ = (call);                                  \
+    if (e_ != hipSuccess) return hip_fail(e_, #call);        \
+  } while (0)
+
+// Launch with optional event bracketing (profiling aid).
+#define BMLP_TIMED(ctx, kind_, s, call)                                         \
+  do {                                                                         \
+    ProfRec *r_ = nullptr;                                                     \
+    if ((ctx)->prof_on && (ctx)->prof_used < (ctx)->prof.size()) {             \
+      r_ = &(ctx)->prof[(ctx)->prof_used++];                                   \
+      r_->kind = (kind_);                                                      \
+      hipError_t ee_ = hipEventRecord(r_->t0, (s));                            \
+      if (ee_ != hipSuccess) return hip_fail(ee_, "hipEventRecord");           \
+    }                                                                          \
+    BMLP_LAUNCH(call);                                                         \
+    if (r_ != nullptr) {                                                       \
+      hipError_t ee_ = hipEventRecord(r_->t1, (s));                            \
+      if (ee_ != hipSuccess) return hip_fail(ee_, "hipEventRecord");           \
+    }                                                                          \
+  } while (0)
+
+inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+inline int words64(int k) { return (k + 63) / 64; }
+
+// Group-size rule of Section 4.3: the divisor of K closest to any value of
+// [75, 105]; among equally close divisors the largest.
+int gamma_star(int k) {
+  int best = 1, best_d = -1;
+  for (int g = 1; g <= k; ++g) {
+    if (k % g) continue;
+    const int d = (g >= 75 && g <= 105) ? 0 : (g < 75 ? 75 - g : g - 105);
+    if (best_d < 0 || d < best_d || (d == best_d && g > best)) {
+      best = g;
+      best_d = d;
+    }
+  }
+  return best;
+}
+
+}  // namespace
+
+int make_plan(const bmlp_config *cfg, Plan *p) {
+  if (cfg == nullptr || p == nullptr || cfg->h_widths == nullptr) return BMLP_EINVAL;
+  if (cfg->n_layers < 1 || cfg->n_layers > BMLP_MAX_LAYERS) return BMLP_ESHAPE;
+  if (cfg->n_classes < 2 || cfg->n_classes > BMLP_MAX_CLASSES) return BMLP_ESHAPE;
+  if (cfg->max_batch < 1 || cfg->max_batch > BMLP_MAX_BATCH) return BMLP_ESHAPE;
+  if (cfg->bound < 1 || cfg->bound > 127 || (cfg->bound & 1) == 0) return BMLP_EINVAL;
+  if (cfg->group_size < 0 || cfg->group_size > BMLP_MAX_GROUP) return BMLP_ESHAPE;
+  if (!(cfg->robustness >= 0.0) || !isfinite(cfg->robustness)) return BMLP_EINVAL;
+  if (cfg->fwd_impl != BMLP_FWD_AUTO && cfg->fwd_impl != BMLP_FWD_POPCOUNT) return BMLP_EINVAL;
+  memset(p, 0, sizeof(*p));
+  p->L = cfg->n_layers;
+  p->c = cfg->n_classes;
+  p->max_batch = cfg->max_batch;
+  p->bound = cfg->bound;
+  p->fwd_impl = cfg->fwd_impl;
+  p->r = cfg->robustness;
+  p->seed = cfg->seed;
+  int kmax = 0;
+  for (int l = 0; l <= p->L; ++l) {
+    const int k = cfg->h_widths[l];
+    if (k < 1 || k > BMLP_MAX_WIDTH) return BMLP_ESHAPE;
+    p->widths[l] = k;
+    if (l > 0 && k > kmax) kmax = k;
+  }
+  const int nb = p->max_batch;
+  size_t so = 0;
+  for (int l = 1; l <= p->L; ++l) {
+    LayerPlan &lp = p->layer[l - 1];
+    lp.k_in = p->widths[l - 1];
+    lp.k_out = p->widths[l];
+    lp.gamma = cfg->group_size > 0 ? cfg->group_size : gamma_star(lp.k_out);
+    if (lp.gamma > BMLP_MAX_GROUP || lp.k_out % lp.gamma != 0) return BMLP_ESHAPE;
+    lp.groups = lp.k_out / lp.gamma;
+    lp.words_in = words64(lp.k_in);
+    lp.words_out = words64(lp.k_out);
+    lp.ld_h = 64 * lp.words_in;
+    const double thr = ceil(p->r * (double)lp.k_out);
+    if (thr > 2147483647.0) return BMLP_EINVAL;
+    lp.robust_thr = (int)thr;
+    lp.off_h = so;
+    so = align256(so + (size_t)lp.k_out * lp.ld_h);
+    lp.off_w = so;
+    so = align256(so + (size_t)lp.k_out * lp.words_in * 8);
+    lp.off_p = so;
+    so = align256(so + (size_t)p->c * lp.words_out * 8);
+  }
+  p->state_bytes = so;
+  size_t wo = 0;
+  for (int l = 1; l <= p->L; ++l) {
+    LayerPlan &lp = p->layer[l - 1];
+    lp.off_a = wo;
+    wo = align256(wo + (size_t)nb * lp.words_out * 8);
+    lp.off_err = wo;
+    wo = align256(wo + (size_t)nb);
+    lp.off_upd = wo;
+    wo = align256(wo + (size_t)nb);
+    lp.off_kstar = wo;
+    wo = align256(wo + (size_t)nb * lp.groups * 2);
+  }
+  p->ldz = 64 * words64(kmax);
+  p->off_z = wo;
+  wo = align256(wo + (size_t)nb * p->ldz * 2);
+  p->off_yhat = wo;
+  wo = align256(wo + (size_t)nb * p->c * 4);
+  p->ws_bytes = wo;
+  return BMLP_OK;
+}
+
+namespace {
+
+inline hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
+
+uint64_t reinforce_threshold(double p_r, int k) {
+  // q = p_r * sqrt(2 / (pi * K)), in this order, in IEEE double.
+  const double pk = 3.14159265358979323846 * (double)k;
+  const double q = p_r * sqrt(2.0 / pk);
+  if (!(q > 0.0)) return 0;
+  const double t = ceil(q * 4294967296.0);
+  if (t >= 4294967296.0) return 4294967296ull;
+  return (uint64_t)t;
+}
+
+int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32_t *yhat_out,
+                   const int32_t *y, int32_t *correct) {
+  const Plan &p = ctx->plan;
+  const uint64_t *a_prev = x;
+  int32_t *yh_ws = reinterpret_cast<int32_t *>(ctx->ws + p.off_yhat);
+  for (int l = 1; l <= p.L; ++l) {
+    const LayerPlan &lp = p.layer[l - 1];
+    const uint64_t *W = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_w);
+    const uint64_t *P = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p);
+    uint64_t *a = reinterpret_cast<uint64_t *>(ctx->ws + lp.off_a);
+    BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s,
+               launch_fwd_popcount(a_prev, lp.words_in, lp.k_in, W, n, lp.k_out, nullptr, 0, a,
+                                   lp.words_out, s));
+    int32_t *yh = yhat_out ? yhat_out + (size_t)(l - 1) * n * p.c : yh_ws;
+    BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s, launch_fill_i32(yh, n * p.c, lp.k_out, s));
+    BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_cls_popcount(a, lp.words_out, lp.k_out, P, n, p.c, yh, p.c, s));
+    if (correct)
+      BMLP_TIMED(ctx, BMLP_KERNEL_SELECT, s, launch_eval_count(yh, p.c, y, n, correct + (l - 1), s));
+    a_prev = a;
+  }
+  return BMLP_OK;
+}
+
+int check_ctx_batch(bmlp_ctx *ctx, const void *x, int n) {
+  if (ctx == nullptr) return BMLP_EINVAL;
+  if (n < 0 || n > ctx->plan.max_batch) return BMLP_ESHAPE;
+  if (n > 0 && x == nullptr) return BMLP_EINVAL;
+  return BMLP_OK;
+}
+
+int setup(const bmlp_config *cfg, void *d_state, void *d_ws, void *stream, bmlp_ctx **out,
+          bool from_h) {
+  if (out == nullptr || d_state == nullptr || d_ws == nullptr) return BMLP_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(d_state) & 255) || (reinterpret_cast<uintptr_t>(d_ws) & 255))
+    return BMLP_ESTATE;
+  bmlp_ctx *ctx = new (std::nothrow) bmlp_ctx;
+  if (ctx == nullptr) return BMLP_EINVAL;
+  const int st = make_plan(cfg, &ctx->plan);
+  if (st != BMLP_OK) {
+    delete ctx;
+    return st;
+  }
+  ctx->state = static_cast<uint8_t *>(d_state);
+  ctx->ws = static_cast<uint8_t *>(d_ws);
+  const Plan &p = ctx->plan;
+  hipStream_t s = as_stream(stream);
+  for (int l = 1; l <= p.L; ++l) {
+    const LayerPlan &lp = p.layer[l - 1];
+    int8_t *H = reinterpret_cast<int8_t *>(ctx->state + lp.off_h);
+    uint64_t *W = reinterpret_cast<uint64_t *>(ctx->state + lp.off_w);
+    uint64_t *P = reinterpret_cast<uint64_t *>(ctx->state + lp.off_p);
+    hipError_t e = launch_init_h(H, lp.ld_h, W, lp.words_in, lp.k_in, lp.k_out, p.seed, l, from_h, s);
+    if (e == hipSuccess && !from_h) e = launch_init_p(P, lp.words_out, lp.k_out, p.c, p.seed, l, s);
+    if (e != hipSuccess) {
+      delete ctx;
+      return hip_fail(e, "init");
+    }
+  }
+  *out = ctx;
+  return BMLP_OK;
+}
+
+}  // namespace
+}  // namespace bmlp
+
+using namespace bmlp;
+
+extern "C" {
+
+size_t bmlp_state_bytes(const bmlp_config *cfg) {
+  Plan p;
+  return make_plan(cfg, &p) == BMLP_OK ? p.state_bytes : 0;
+}
+
+size_t bmlp_workspace_bytes(const bmlp_config *cfg) {
+  Plan p;
+  return make_plan(cfg, &p) == BMLP_OK ? p.ws_bytes : 0;
+}
+
+int bmlp_describe(const bmlp_config *cfg, int32_t l, bmlp_layer_info *info) {
+  if (info == nullptr) return BMLP_EINVAL;
+  Plan p;
+  const int st = make_plan(cfg, &p);
+  if (st != BMLP_OK) return st;
+  if (l < 1 || l > p.L) return BMLP_ESHAPE;
+  const LayerPlan &lp = p.layer[l - 1];
+  info->k_in = lp.k_in;
+  info->k_out = lp.k_out;
+  info->gamma = lp.gamma;
+  info->groups = lp.groups;
+  info->words_in = lp.words_in;
+  info->words_out = lp.words_out;
+  info->ld_h = lp.ld_h;
+  info->robust_thr = lp.robust_thr;
+  info->off_h = lp.off_h;
+  info->off_w = lp.off_w;
+  info->off_p = lp.off_p;
+  info->off_a = lp.off_a;
+  info->off_err = lp.off_err;
+  info->off_upd = lp.off_upd;
+  info->off_kstar = lp.off_kstar;
+  return BMLP_OK;
+}
+
+uint64_t bmlp_reinforce_threshold(double p_r, int32_t k_l) {
+  if (k_l < 1) return 0;
+  return reinforce_threshold(p_r, k_l);
+}
+
+int bmlp_init(const bmlp_config *cfg, void *d_state, void *d_workspace, void *stream,
+              bmlp_ctx **out) {
+  return setup(cfg, d_state, d_workspace, stream, out, false);
+}
+
+int bmlp_attach(const bmlp_config *cfg, void *d_state, void *d_workspace, void *stream,
+                bmlp_ctx **out) {
+  return setup(cfg, d_state, d_workspace, stream, out, true);
+}
+
+int bmlp_pack(const int8_t *d_pm1, int32_t n, int32_t K, uint64_t *d_bits, void *stream) {
+  if (n < 0 || K < 1 || n > 65535) return BMLP_ESHAPE;
+  if (n > 0 && (d_pm1 == nullptr || d_bits == nullptr)) return BMLP_EINVAL;
+  BMLP_LAUNCH(launch_pack(d_pm1, n, K, d_bits, as_stream(stream)));
+  return BMLP_OK;
+}
+
+int bmlp_forward(bmlp_ctx *ctx, const uint64_t *d_x, int32_t n, int32_t *d_yhat, void *stream) {
+  int st = check_ctx_batch(ctx, d_x, n);
+  if (st != BMLP_OK) return st;
+  if (n > 0 && d_yhat == nullptr) return BMLP_EINVAL;
+  if (n == 0) return BMLP_OK;
+  return forward_layers(ctx, d_x, n, as_stream(stream), d_yhat, nullptr, nullptr);
+}
+
+int bmlp_eval(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int32_t n,
+              int32_t *d_correct, void *stream) {
+  int st = check_ctx_batch(ctx, d_x, n);
+  if (st != BMLP_OK) return st;
+  if (n > 0 && (d_y == nullptr || d_correct == nullptr)) return BMLP_EINVAL;
+  if (n == 0) return BMLP_OK;
+  return forward_layers(ctx, d_x, n, as_stream(stream), nullptr, d_y, d_correct);
+}
+
+int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int32_t n,
+                    uint64_t step, double p_r, int32_t *d_stats, void *stream) {
+  int st = check_ctx_batch(ctx, d_x, n);
+  if (st != BMLP_OK) return st;
+  if (d_stats == nullptr || (n > 0 && d_y == nullptr)) return BMLP_EINVAL;
+  if (!(p_r >= 0.0) || !isfinite(p_r)) return BMLP_EINVAL;
+  const Plan &p = ctx->plan;
+  hipStream_t s = as_stream(stream);
+  BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s, launch_fill_i32(d_stats, 4 * p.L, 0, s));
+  if (n == 0) return BMLP_OK;
+  const uint64_t *a_prev = d_x;
+  int16_t *z = reinterpret_cast<int16_t *>(ctx->ws + p.off_z);
+  int32_t *yh = reinterpret_cast<int32_t *>(ctx->ws + p.off_yhat);
+  for (int l = 1; l <= p.L; ++l) {
+    const LayerPlan &lp = p.layer[l - 1];
+    int8_t *H = reinterpret_cast<int8_t *>(ctx->state + lp.off_h);
+    uint64_t *W = reinterpret_cast<uint64_t *>(ctx->state + lp.off_w);
+    const uint64_t *P = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p);
+    uint64_t *a = reinterpret_cast<uint64_t *>(ctx->ws + lp.off_a);
+    uint8_t *err = ctx->ws + lp.off_err;
+    uint8_t *upd = ctx->ws + lp.off_upd;
+    int16_t *kstar = reinterpret_cast<int16_t *>(ctx->ws + lp.off_kstar);
+    int32_t *stats = d_stats + 4 * (l - 1);
+
+    // Algorithm 1: z_l, a_l, y_hat_l
+    BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s,
+               launch_fwd_popcount(a_prev, lp.words_in, lp.k_in, W, n, lp.k_out, z, p.ldz, a,
+                                   lp.words_out, s));
+    BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s, launch_fill_i32(yh, n * p.c, lp.k_out, s));
+    BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_cls_popcount(a, lp.words_out, lp.k_out, P, n, p.c, yh, p.c, s));
+    // Eq. 1, robustness, M_l; Algorithm 2
+    LossSelectArgs ls{};
+    ls.yhat = yh; ls.c = p.c;
+    ls.z = z; ls.ldz = p.ldz;
+    ls.P = P; ls.words_out = lp.words_out;
+    ls.y = d_y; ls.n = n;
+    ls.k_out = lp.k_out; ls.gamma = lp.gamma; ls.groups = lp.groups; ls.thr = lp.robust_thr;
+    ls.err = err; ls.upd = upd; ls.kstar = kstar; ls.stats = stats;
+    BMLP_TIMED(ctx, BMLP_KERNEL_SELECT, s, launch_loss_select(ls, s));
+    // Algorithm 3
+    const uint64_t T = reinforce_threshold(p_r, lp.k_out);
+    UpdateArgs u{};
+    u.H = H; u.ld_h = lp.ld_h;
+    u.W = W; u.words_in = lp.words_in;
+    u.a_prev = a_prev;
+    u.kstar = kstar; u.groups = lp.groups; u.gamma = lp.gamma;
+    u.P = P; u.words_out = lp.words_out;
+    u.y = d_y; u.n = n; u.c = p.c;
+    u.k_in = lp.k_in; u.k_out = lp.k_out; u.bound = p.bound;
+    u.t_hi = (uint32_t)(T >> 24); u.t_lo = (uint32_t)(T & 0xFFFFFFu);
+    u.seed = p.seed; u.layer = l; u.step = (uint32_t)step;
+    u.stats = stats;
+    BMLP_TIMED(ctx, BMLP_KERNEL_UPDATE, s, launch_update(u, s));
+    a_prev = a;
+  }
+  return BMLP_OK;
+}
+
+int bmlp_layer_views(bmlp_ctx *ctx, int32_t l, int8_t **d_h, uint64_t **d_w, uint64_t **d_p) {
+  if (ctx == nullptr) return BMLP_EINVAL;
+  if (l < 1 || l > ctx->plan.L) return BMLP_ESHAPE;
+  const LayerPlan &lp = ctx->plan.layer[l - 1];
+  if (d_h) *d_h = reinterpret_cast<int8_t *>(ctx->state + lp.off_h);
+  if (d_w) *d_w = reinterpret_cast<uint64_t *>(ctx->state + lp.off_w);
+  if (d_p) *d_p = reinterpret_cast<uint64_t *>(ctx->state + lp.off_p);
+  return BMLP_OK;
+}
+
+int bmlp_step_trace(bmlp_ctx *ctx, int32_t l, const uint64_t **d_a, const uint8_t **d_err,
+                    const uint8_t **d_upd, const int16_t **d_kstar) {
+  if (ctx == nullptr) return BMLP_EINVAL;
+  if (l < 1 || l > ctx->plan.L) return BMLP_ESHAPE;
+  const LayerPlan &lp = ctx->plan.layer[l - 1];
+  if (d_a) *d_a = reinterpret_cast<const uint64_t *>(ctx->ws + lp.off_a);
+  if (d_err) *d_err = ctx->ws + lp.off_err;
+  if (d_upd) *d_upd = ctx->ws + lp.off_upd;
+  if (d_kstar) *d_kstar = reinterpret_cast<const int16_t *>(ctx->ws + lp.off_kstar);
+  return BMLP_OK;
+}
+
+const char *bmlp_status_string(int status) {
+  switch (status) {
+    case BMLP_OK: return "ok";
+    case BMLP_EINVAL: return "invalid argument";
+    case BMLP_ESHAPE: return "size out of range";
+    case BMLP_EHIP: return "HIP launch failed";
+    case BMLP_ESTATE: return "misaligned state or workspace buffer";
+    default: return "unknown status";
+  }
+}
+
+const char *bmlp_last_error(void) { return g_last_error; }
+
+static void prof_release(bmlp_ctx *ctx) {
+  for (ProfRec &r : ctx->prof) {
+    if (r.t0) (void)hipEventDestroy(r.t0);
+    if (r.t1) (void)hipEventDestroy(r.t1);
+  }
+  ctx->prof.clear();
+  ctx->prof_used = 0;
+  ctx->prof_on = false;
+}
+
+int bmlp_profile_start(bmlp_ctx *ctx, int32_t max_launches) {
+  if (ctx == nullptr) return BMLP_EINVAL;
+  if (max_launches < 1 || max_launches > (1 << 20)) return BMLP_ESHAPE;
+  prof_release(ctx);
+  ctx->prof.resize((size_t)max_launches, ProfRec{0, nullptr, nullptr});
+  for (ProfRec &r : ctx->prof) {
+    hipError_t e = hipEventCreate(&r.t0);
+    if (e == hipSuccess) e = hipEventCreate(&r.t1);
+    if (e != hipSuccess) {
+      prof_release(ctx);
+      return hip_fail(e, "hipEventCreate");
+    }
+  }
+  ctx->prof_on = true;
+  return BMLP_OK;
+}
+
+int bmlp_profile_stop(bmlp_ctx *ctx, double *h_ms, int64_t *h_launches) {
+  if (ctx == nullptr) return BMLP_EINVAL;
+  double ms[BMLP_KERNEL_KINDS] = {0};
+  int64_t cnt[BMLP_KERNEL_KINDS] = {0};
+  int status = BMLP_OK;
+  if (ctx->prof_used > 0) {
+    hipError_t e = hipEventSynchronize(ctx->prof[ctx->prof_used - 1].t1);
+    if (e != hipSuccess) status = hip_fail(e, "hipEventSynchronize");
+    for (size_t i = 0; status == BMLP_OK && i < ctx->prof_used; ++i) {
+      float t = 0.f;
+      e = hipEventElapsedTime(&t, ctx->prof[i].t0, ctx->prof[i].t1);
+      if (e != hipSuccess) {
+        status = hip_fail(e, "hipEventElapsedTime");
+        break;
+      }
+      ms[ctx->prof[i].kind] += t;
+      cnt[ctx->prof[i].kind] += 1;
+    }
+  }
+  prof_release(ctx);
+  for (int k = 0; k < BMLP_KERNEL_KINDS; ++k) {
+    if (h_ms) h_ms[k] = ms[k];
+    if (h_launches) h_launches[k] = cnt[k];
+  }
+  return status;
+}
+
+void bmlp_destroy(bmlp_ctx *ctx) {
+  if (ctx) prof_release(ctx);
+  delete ctx;
+}
+
+}  // extern "C"

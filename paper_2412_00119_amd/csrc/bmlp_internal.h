@@ -1,0 +1,102 @@
+// Internal declarations shared by the host library and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "bmlp.h"
+
+namespace bmlp {
+
+// Philox stream ids of the method's random draws (counter word 3).
+enum : uint32_t {
+  kStreamHInit = 1,     // H_l initial signs
+  kStreamPInit = 2,     // P_l entries
+  kStreamCoarse = 3,    // reinforcement: top byte of the 32-bit draw
+  kStreamFine = 4,      // reinforcement: low 24 bits of the 32-bit draw
+};
+
+struct LayerPlan {
+  int k_in, k_out, gamma, groups;
+  int words_in, words_out;   // uint64 words per bit row of a_{l-1} / a_l
+  int ld_h;                  // bytes per H row, multiple of 64
+  int robust_thr;            // ceil(r K_l)
+  size_t off_h, off_w, off_p;
+  size_t off_a, off_err, off_upd, off_kstar;
+};
+
+struct Plan {
+  int L, c, max_batch, bound, fwd_impl;
+  double r;
+  uint64_t seed;
+  int widths[BMLP_MAX_LAYERS + 1];
+  LayerPlan layer[BMLP_MAX_LAYERS];   // layer[l-1] describes layer l
+  int ldz;                            // int16 elements per row of the z scratch
+  size_t off_z, off_yhat;             // shared scratch in the workspace
+  size_t state_bytes, ws_bytes;
+};
+
+// Validates cfg and fills plan; returns a BMLP_* status.
+int make_plan(const bmlp_config *cfg, Plan *plan);
+
+// ---------------------------------------------------------------------------
+// Launchers (each returns hipSuccess or the launch error).
+// ---------------------------------------------------------------------------
+
+hipError_t launch_pack(const int8_t *x, int n, int K, uint64_t *bits, hipStream_t s);
+
+// H_l and W_l of one layer from Philox stream 1 (init) or W_l from the H_l in
+// place (attach); P_l from stream 2.
+hipError_t launch_init_h(int8_t *H, int ld_h, uint64_t *W, int words_in, int k_in, int k_out,
+                         uint64_t seed, int layer, bool from_h, hipStream_t s);
+hipError_t launch_init_p(uint64_t *P, int words_out, int k_out, int c, uint64_t seed, int layer,
+                         hipStream_t s);
+
+hipError_t launch_fill_i32(int32_t *p, int count, int32_t value, hipStream_t s);
+hipError_t launch_fill_rows_i32(int32_t *p, int rows, int cols, int ld, int32_t value,
+                                hipStream_t s);
+
+// Hidden layer forward: z = K_in - 2 popc(a_prev ^ W) -> z (int16 [n][ldz],
+// optional) and a = (z >= 0) bits [n][words_out].
+hipError_t launch_fwd_popcount(const uint64_t *a_prev, int words_in, int k_in, const uint64_t *W,
+                               int n, int k_out, int16_t *z, int ldz, uint64_t *a_out,
+                               int words_out, hipStream_t s);
+
+// Local classifier: out[m][c] += -2 popc(a ^ P_c); out must hold K_l first.
+hipError_t launch_cls_popcount(const uint64_t *a, int words, int k, const uint64_t *P, int n,
+                               int c, int32_t *out, int ldo, hipStream_t s);
+
+// 01-loss, margin, M and the easiest wrong perceptron per group.
+struct LossSelectArgs {
+  const int32_t *yhat; int c;
+  const int16_t *z; int ldz;
+  const uint64_t *P; int words_out;
+  const int32_t *y; int n;
+  int k_out, gamma, groups, thr;
+  uint8_t *err, *upd;
+  int16_t *kstar;
+  int32_t *stats;          // this layer's [4]
+};
+hipError_t launch_loss_select(const LossSelectArgs &a, hipStream_t s);
+
+// correct[0] += #(argmax yhat == y)
+hipError_t launch_eval_count(const int32_t *yhat, int c, const int32_t *y, int n, int32_t *correct,
+                             hipStream_t s);
+
+// Clipped-Perceptron increments + reinforcement + clip + re-sign of one layer.
+struct UpdateArgs {
+  int8_t *H; int ld_h;
+  uint64_t *W; int words_in;
+  const uint64_t *a_prev;
+  const int16_t *kstar; int groups, gamma;
+  const uint64_t *P; int words_out;
+  const int32_t *y; int n, c;
+  int k_in, k_out, bound;
+  uint32_t t_hi, t_lo;     // T_l >> 24 (0..256) and T_l & 0xFFFFFF
+  uint64_t seed; int layer; uint32_t step;
+  int32_t *stats;          // this layer's [4]; reads [1] (|M|), adds [3]
+};
+hipError_t launch_update(const UpdateArgs &a, hipStream_t s);
+
+}  // namespace bmlp

@@ -1,0 +1,133 @@
+// Local error signal and perceptron selection (Algorithm 1 01-loss and
+// robustness test, Eq. 1; Algorithm 2 easiest-perceptron choice).
+//
+// One wave per pattern.  The wave finds the first argmax of y_hat and the two
+// largest values (tau = top1 - top2, 0 on a tie), sets err = (pred != y) and
+// upd = err or tau < ceil(r K_l).  For a pattern in M it then takes, in every
+// group of gamma contiguous perceptrons, the one with the largest negative
+// stability delta_k = z_k rho^{y}_k, i.e. the smallest |z_k| among those whose
+// sign disagrees with rho^{y}_k, lowest k on ties; delta = 0 is not eligible.
+#include <limits.h>
+
+#include "bmlp_internal.h"
+
+namespace bmlp {
+namespace {
+
+struct Top2 {
+  int v1, i1, v2;
+};
+
+__device__ __forceinline__ Top2 merge(Top2 a, Top2 b) {
+  Top2 r;
+  if (a.v1 > b.v1 || (a.v1 == b.v1 && a.i1 < b.i1)) {
+    r.v1 = a.v1;
+    r.i1 = a.i1;
+  } else {
+    r.v1 = b.v1;
+    r.i1 = b.i1;
+  }
+  // second largest value of the union of the two multisets
+  r.v2 = max(min(a.v1, b.v1), max(a.v2, b.v2));
+  return r;
+}
+
+__device__ __forceinline__ Top2 wave_top2(const int32_t *row, int c, int lane) {
+  Top2 t{INT_MIN, INT_MAX, INT_MIN};
+  for (int cl = lane; cl < c; cl += 64) {
+    const int v = row[cl];
+    if (v > t.v1) {
+      t.v2 = t.v1;
+      t.v1 = v;
+      t.i1 = cl;
+    } else if (v > t.v2) {
+      t.v2 = v;
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    Top2 o;
+    o.v1 = __shfl_xor(t.v1, off, 64);
+    o.i1 = __shfl_xor(t.i1, off, 64);
+    o.v2 = __shfl_xor(t.v2, off, 64);
+    t = merge(t, o);
+  }
+  return t;
+}
+
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// Grid: ceil(n / 4) blocks of 256 threads, one wave per pattern.
+__global__ __launch_bounds__(256) void loss_select_kernel(LossSelectArgs p) {
+  const int mu = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (mu >= p.n) return;
+  const Top2 t = wave_top2(p.yhat + (size_t)mu * p.c, p.c, lane);
+  const int label = p.y[mu];
+  const int yl = min(max(label, 0), p.c - 1);      // stay inside P on a bad label
+  const bool err = t.i1 != label;
+  const bool upd = err || (t.v1 - t.v2) < p.thr;
+  int nsel = 0;
+  int16_t *ks = p.kstar + (size_t)mu * p.groups;
+  if (upd) {
+    const int16_t *zr = p.z + (size_t)mu * p.ldz;
+    const uint64_t *rho = p.P + (size_t)yl * p.words_out;
+    for (int g = lane; g < p.groups; g += 64) {
+      int best = -1, bestabs = INT_MAX;
+      const int k0 = g * p.gamma;
+      for (int e = 0; e < p.gamma; ++e) {
+        const int k = k0 + e;
+        const int zz = zr[k];
+        const bool rpos = (rho[k >> 6] >> (k & 63)) & 1ull;
+        const bool wrong = rpos ? (zz < 0) : (zz > 0);
+        const int a = zz < 0 ? -zz : zz;
+        if (wrong && a < bestabs) {
+          bestabs = a;
+          best = e;
+        }
+      }
+      ks[g] = (int16_t)best;
+      nsel += best >= 0;
+    }
+  } else {
+    for (int g = lane; g < p.groups; g += 64) ks[g] = (int16_t)-1;
+  }
+  nsel = wave_sum(nsel);
+  if (lane == 0) {
+    p.err[mu] = err ? 1 : 0;
+    p.upd[mu] = upd ? 1 : 0;
+    if (err) atomicAdd(p.stats + 0, 1);
+    if (upd) atomicAdd(p.stats + 1, 1);
+    if (nsel) atomicAdd(p.stats + 2, nsel);
+  }
+}
+
+__global__ __launch_bounds__(256) void eval_count_kernel(const int32_t *yhat, int c, const int32_t *y,
+                                                         int n, int32_t *correct) {
+  const int mu = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (mu >= n) return;
+  const Top2 t = wave_top2(yhat + (size_t)mu * c, c, lane);
+  if (lane == 0 && t.i1 == y[mu]) atomicAdd(correct, 1);
+}
+
+}  // namespace
+
+hipError_t launch_loss_select(const LossSelectArgs &a, hipStream_t s) {
+  if (a.n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(loss_select_kernel, dim3((a.n + 3) / 4), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_eval_count(const int32_t *yhat, int c, const int32_t *y, int n, int32_t *correct,
+                             hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(eval_count_kernel, dim3((n + 3) / 4), dim3(256), 0, s, yhat, c, y, n, correct);
+  return hipGetLastError();
+}
+
+}  // namespace bmlp

@@ -1,0 +1,120 @@
+// Setup kernels: bit packing of ±1 inputs, state initialisation, fills.
+#include "bmlp_internal.h"
+#include "philox.h"
+
+namespace bmlp {
+namespace {
+
+// One wave per 64-value chunk of a row: lane i tests value (w*64 + i) and the
+// wave ballot is the packed word.  Grid: (ceil(words/4), n), 256 threads.
+__global__ __launch_bounds__(256) void pack_kernel(const int8_t *__restrict__ x, int n, int K,
+                                                   int words, uint64_t *__restrict__ bits) {
+  const int row = blockIdx.y;
+  const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= n || w >= words) return;     // whole wave leaves together
+  const int col = w * 64 + lane;
+  const bool pos = col < K && x[(size_t)row * K + col] > 0;
+  const uint64_t m = __ballot(pos);
+  if (lane == 0) bits[(size_t)row * words + w] = m;
+}
+
+// Bit (j & 127) of Philox block j >> 7 of the given layer/stream at step 0.
+__device__ __forceinline__ bool stream_bit(uint64_t j, uint64_t seed, int layer, uint32_t stream) {
+  const U32x4 v = philox4x32_10((uint32_t)(j >> 7), (uint32_t)(layer - 1), 0u, stream,
+                                (uint32_t)seed, (uint32_t)(seed >> 32));
+  const uint32_t b = (uint32_t)(j & 127);
+  return (pick_word(v, b >> 5) >> (b & 31)) & 1u;
+}
+
+// Grid: (ceil(ld_h / 256), k_out).  Thread = one column of one H row; each
+// wave covers 64 aligned columns and ballots the W word.
+__global__ __launch_bounds__(256) void init_h_kernel(int8_t *__restrict__ H, int ld_h,
+                                                     uint64_t *__restrict__ W, int words_in,
+                                                     int k_in, int k_out, uint64_t seed, int layer,
+                                                     int from_h) {
+  const int k = blockIdx.y;
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (k >= k_out || i >= ld_h) return;    // ld_h is a multiple of 64: waves stay whole
+  int8_t h = 0;
+  if (from_h) {
+    h = i < k_in ? H[(size_t)k * ld_h + i] : (int8_t)0;
+  } else if (i < k_in) {
+    const uint64_t j = (uint64_t)k * (uint64_t)k_in + (uint64_t)i;
+    h = stream_bit(j, seed, layer, kStreamHInit) ? (int8_t)1 : (int8_t)-1;
+  }
+  if (!from_h) H[(size_t)k * ld_h + i] = h;
+  const uint64_t m = __ballot(h > 0);
+  const int w = i >> 6;
+  if ((threadIdx.x & 63) == 0 && w < words_in) W[(size_t)k * words_in + w] = m;
+}
+
+// Grid: (ceil(words_out / 4), c).  One wave per 64 classifier entries.
+__global__ __launch_bounds__(256) void init_p_kernel(uint64_t *__restrict__ P, int words_out,
+                                                     int k_out, int c, uint64_t seed, int layer) {
+  const int cls = blockIdx.y;
+  const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (cls >= c || w >= words_out) return;
+  const int k = w * 64 + lane;
+  bool bit = false;
+  if (k < k_out) {
+    const uint64_t j = (uint64_t)cls * (uint64_t)k_out + (uint64_t)k;
+    bit = stream_bit(j, seed, layer, kStreamPInit);
+  }
+  const uint64_t m = __ballot(bit);
+  if (lane == 0) P[(size_t)cls * words_out + w] = m;
+}
+
+__global__ __launch_bounds__(256) void fill_i32_kernel(int32_t *p, int count, int32_t v) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < count) p[i] = v;
+}
+
+__global__ __launch_bounds__(256) void fill_rows_kernel(int32_t *p, int rows, int cols, int ld,
+                                                        int32_t v) {
+  const int r = blockIdx.y;
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (r < rows && c < cols) p[(size_t)r * ld + c] = v;
+}
+
+inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+}  // namespace
+
+hipError_t launch_pack(const int8_t *x, int n, int K, uint64_t *bits, hipStream_t s) {
+  const int words = cdiv(K, 64);
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(pack_kernel, dim3(cdiv(words, 4), n), dim3(256), 0, s, x, n, K, words, bits);
+  return hipGetLastError();
+}
+
+hipError_t launch_init_h(int8_t *H, int ld_h, uint64_t *W, int words_in, int k_in, int k_out,
+                         uint64_t seed, int layer, bool from_h, hipStream_t s) {
+  hipLaunchKernelGGL(init_h_kernel, dim3(cdiv(ld_h, 256), k_out), dim3(256), 0, s, H, ld_h, W,
+                     words_in, k_in, k_out, seed, layer, from_h ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_init_p(uint64_t *P, int words_out, int k_out, int c, uint64_t seed, int layer,
+                         hipStream_t s) {
+  hipLaunchKernelGGL(init_p_kernel, dim3(cdiv(words_out, 4), c), dim3(256), 0, s, P, words_out,
+                     k_out, c, seed, layer);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_i32(int32_t *p, int count, int32_t value, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(cdiv(count, 256)), dim3(256), 0, s, p, count, value);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_rows_i32(int32_t *p, int rows, int cols, int ld, int32_t value,
+                                hipStream_t s) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_rows_kernel, dim3(cdiv(cols, 256), rows), dim3(256), 0, s, p, rows, cols,
+                     ld, value);
+  return hipGetLastError();
+}
+
+}  // namespace bmlp

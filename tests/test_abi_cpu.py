@@ -1,0 +1,115 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every function include/bmlp.h declares, and its host logic (configuration
+checks, group-size rule, thresholds, layout) behaves as documented.  The
+group-size rule and thresholds are compared with the oracle and the paper's
+worked examples."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle.bmlp as ob
+from paper_2412_00119_amd import bmlp as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "bmlp.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = re.findall(r"\b(bmlp_[a-z_]+)\s*\(", src)
+    return sorted(set(names))
+
+
+def test_every_declared_symbol_is_exported():
+    L = B.lib()
+    names = declared_functions()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings():
+    for st in (B.BMLP_OK, B.BMLP_EINVAL, B.BMLP_ESHAPE, B.BMLP_EHIP, B.BMLP_ESTATE):
+        assert B.status_string(st) != "unknown status"
+    assert B.status_string(99) == "unknown status"
+
+
+@pytest.mark.parametrize("k", [525, 2025, 4096, 8192, 1024, 256, 97, 210, 35, 135])
+def test_gamma_star_matches_oracle(k):
+    cfg = B.make_config((100, k), 10, 15, 8, group_size=0)
+    assert B.bmlp_describe(cfg, 1).gamma == ob.gamma_star(k)
+
+
+def test_gamma_star_paper_examples():
+    for k, g in [(525, 105), (2025, 81)]:
+        info = B.bmlp_describe(B.make_config((64, k), 10, 15, 8, group_size=0), 1)
+        assert (info.gamma, info.groups) == (g, k // g)
+
+
+@pytest.mark.parametrize("p_r,k", [(0.5, 4096), (0.5, 256), (0.5, 784), (1e-9, 100), (0.0, 10),
+                                   (1e6, 64), (0.37, 2048), (0.5 * 0.81 ** 0.5, 1024)])
+def test_reinforce_threshold_matches_oracle(p_r, k):
+    assert B.bmlp_reinforce_threshold(p_r, k) == ob.reinforce_threshold(p_r, k)
+
+
+@pytest.mark.parametrize("r,k", [(0.25, 4096), (0.25, 35), (0.0, 100), (0.3, 1000), (1.0 / 3, 999)])
+def test_robust_threshold_matches_oracle(r, k):
+    info = B.bmlp_describe(B.make_config((50, k), 10, 15, 8, group_size=1, robustness=r), 1)
+    assert info.robust_thr == ob.robustness_threshold(r, k)
+
+
+def test_layout_is_aligned_and_disjoint():
+    cfg = B.make_config((784, 1024, 1024), 10, 127, 256)
+    sb = B.bmlp_state_bytes(cfg)
+    wb = B.bmlp_workspace_bytes(cfg)
+    spans = []
+    for l in (1, 2):
+        i = B.bmlp_describe(cfg, l)
+        assert i.ld_h % 64 == 0 and i.ld_h >= i.k_in
+        for off in (i.off_h, i.off_w, i.off_p, i.off_a, i.off_err, i.off_upd, i.off_kstar):
+            assert off % 256 == 0
+        spans += [(i.off_h, i.off_h + i.k_out * i.ld_h), (i.off_w, i.off_w + i.k_out * i.words_in * 8),
+                  (i.off_p, i.off_p + 10 * i.words_out * 8)]
+    spans.sort()
+    for (a0, a1), (b0, b1) in zip(spans, spans[1:]):
+        assert a1 <= b0
+    assert spans[-1][1] <= sb and wb > 0
+
+
+@pytest.mark.parametrize("kw", [
+    dict(widths=(784,), n_classes=10, bound=15, max_batch=8),             # no layer
+    dict(widths=(784, 256), n_classes=1, bound=15, max_batch=8),          # one class
+    dict(widths=(784, 256), n_classes=10, bound=14, max_batch=8),         # even bound
+    dict(widths=(784, 256), n_classes=10, bound=129, max_batch=8),        # bound > 127
+    dict(widths=(784, 250), n_classes=10, bound=15, max_batch=8),         # 64 does not divide 250
+    dict(widths=(784, 256), n_classes=10, bound=15, max_batch=0),
+    dict(widths=(784, 256), n_classes=10, bound=15, max_batch=B.MAX_BATCH + 1),
+    dict(widths=(0, 256), n_classes=10, bound=15, max_batch=8),
+    dict(widths=(784, 40000), n_classes=10, bound=15, max_batch=8, group_size=100),
+    dict(widths=(784, 256), n_classes=10, bound=15, max_batch=8, robustness=-1.0),
+    dict(widths=(784, 256), n_classes=10, bound=15, max_batch=8, fwd_impl=7),
+])
+def test_invalid_configs_rejected(kw):
+    cfg = B.make_config(**kw)
+    assert B.bmlp_state_bytes(cfg) == 0
+    assert B.bmlp_workspace_bytes(cfg) == 0
+    ctx = ctypes.c_void_p()
+    # valid-looking aligned device pointers: rejection happens before any launch
+    st = B.lib().bmlp_init(ctypes.byref(cfg), 1 << 20, 1 << 21, None, ctypes.byref(ctx))
+    assert st in (B.BMLP_EINVAL, B.BMLP_ESHAPE)
+    assert ctx.value is None
+
+
+def test_null_and_misaligned_buffers_rejected():
+    cfg = B.make_config((784, 256), 10, 15, 8)
+    ctx = ctypes.c_void_p()
+    L = B.lib()
+    assert L.bmlp_init(ctypes.byref(cfg), None, 1 << 20, None, ctypes.byref(ctx)) == B.BMLP_EINVAL
+    assert L.bmlp_init(ctypes.byref(cfg), (1 << 20) + 8, 1 << 21, None, ctypes.byref(ctx)) == B.BMLP_ESTATE
+    assert L.bmlp_init(ctypes.byref(cfg), 1 << 20, (1 << 21) + 128, None, ctypes.byref(ctx)) == B.BMLP_ESTATE
+    assert L.bmlp_init(None, 1 << 20, 1 << 21, None, ctypes.byref(ctx)) == B.BMLP_EINVAL
+    assert L.bmlp_train_step(None, 1 << 20, 1 << 21, 4, 0, 0.5, 1 << 22, None) == B.BMLP_EINVAL
+    assert L.bmlp_pack(None, 4, 10, None, None) == B.BMLP_EINVAL
+    assert L.bmlp_pack(None, 0, 0, None, None) == B.BMLP_ESHAPE
