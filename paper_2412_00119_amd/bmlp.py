@@ -219,7 +219,10 @@ class BMLP:
                  fwd_impl: int = BMLP_FWD_AUTO, device="cuda", state=None):
         import torch
         self.torch = torch
-        self.device = torch.device(device)
+        dev = torch.device(device)
+        if dev.type == "cuda" and dev.index is None:
+            dev = torch.device("cuda", torch.cuda.current_device())
+        self.device = dev
         self.widths = tuple(int(w) for w in widths)
         self.n_layers = len(self.widths) - 1
         self.n_classes = int(n_classes)
