@@ -100,6 +100,9 @@ def main():
     ap.add_argument("--workload", default="bmlp-3072-4096x4")
     ap.add_argument("--fwd-impl", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mb", type=int, default=0,
+                    help="run one plain device-to-device copy of this many MiB before timing "
+                         "(a known-size kernel for calibrating HBM byte counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -115,6 +118,15 @@ def main():
     if not torch.cuda.is_available():
         log("no GPU visible")
         sys.exit(1)
+    if args.calib_copy_mb > 0:
+        nbytes = args.calib_copy_mb << 20
+        src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy: {nbytes} bytes read, {nbytes} bytes written")
+        del src, dst
     w = synth.WORKLOADS[args.workload]
     net = B.BMLP(w.widths, w.n_classes, w.bound, w.batch, w.group_size, w.robustness,
                  w.seed_model, fwd_impl=args.fwd_impl)

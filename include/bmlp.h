@@ -117,7 +117,7 @@ typedef struct bmlp_config {
  *                    a_l    uint64 [max_batch][words_out]
  *                    err_l  uint8  [max_batch]   01-loss
  *                    upd_l  uint8  [max_batch]   1 = pattern in M_l
- *                    kstar_l int16 [max_batch][groups]  easiest wrong
+ *                    kstar_l int16 [groups][max_batch]  easiest wrong
  *                           perceptron of each group as an offset in the
  *                           group; -1 when the group has none or the pattern
  *                           is not in M_l (the pairs of U_l, Algorithm 2).
@@ -195,7 +195,7 @@ int bmlp_eval(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int32_t n,
 int bmlp_layer_views(bmlp_ctx *ctx, int32_t l, int8_t **d_h, uint64_t **d_w, uint64_t **d_p);
 
 /* Device pointers to the last train step's per-layer trace in the workspace
- * (layouts in bmlp_layer_info). */
+ * (layouts in bmlp_layer_info).  bmlp_forward and bmlp_eval overwrite a_l. */
 int bmlp_step_trace(bmlp_ctx *ctx, int32_t l, const uint64_t **d_a, const uint8_t **d_err,
                     const uint8_t **d_upd, const int16_t **d_kstar);
 

@@ -327,5 +327,7 @@ class BMLP:
             "a": self._view(self.ws, i.off_a, n * i.words_out * 8, t.int64, (n, i.words_out)),
             "err": self._view(self.ws, i.off_err, n, t.uint8, (n,)),
             "upd": self._view(self.ws, i.off_upd, n, t.uint8, (n,)),
-            "kstar": self._view(self.ws, i.off_kstar, n * i.groups * 2, t.int16, (n, i.groups)),
+            # stored group-major [groups][max_batch]; returned as [n][groups]
+            "kstar": self._view(self.ws, i.off_kstar, self.max_batch * i.groups * 2, t.int16,
+                                (i.groups, self.max_batch))[:, :n].t(),
         }

@@ -338,23 +338,34 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
     ls.P = P; ls.words_out = lp.words_out;
     ls.y = d_y; ls.n = n;
     ls.k_out = lp.k_out; ls.gamma = lp.gamma; ls.groups = lp.groups; ls.thr = lp.robust_thr;
-    ls.err = err; ls.upd = upd; ls.kstar = kstar; ls.stats = stats;
+    ls.err = err; ls.upd = upd; ls.kstar = kstar; ls.ldk = p.max_batch; ls.stats = stats;
     BMLP_TIMED(ctx, BMLP_KERNEL_SELECT, s, launch_loss_select(ls, s));
-    // Algorithm 3
-    const uint64_t T = reinforce_threshold(p_r, lp.k_out);
-    UpdateArgs u{};
-    u.H = H; u.ld_h = lp.ld_h;
-    u.W = W; u.words_in = lp.words_in;
-    u.a_prev = a_prev;
-    u.kstar = kstar; u.groups = lp.groups; u.gamma = lp.gamma;
-    u.P = P; u.words_out = lp.words_out;
-    u.y = d_y; u.n = n; u.c = p.c;
-    u.k_in = lp.k_in; u.k_out = lp.k_out; u.bound = p.bound;
-    u.t_hi = (uint32_t)(T >> 24); u.t_lo = (uint32_t)(T & 0xFFFFFFu);
-    u.seed = p.seed; u.layer = l; u.step = (uint32_t)step;
-    u.stats = stats;
-    BMLP_TIMED(ctx, BMLP_KERNEL_UPDATE, s, launch_update(u, s));
     a_prev = a;
+  }
+  // Algorithm 3 for every layer (each layer's forward above used its
+  // pre-step weights; the updates touch only H_l and W_l).
+  UpdateBatch ub{};
+  ub.y = d_y; ub.n = n; ub.ldk = p.max_batch; ub.c = p.c; ub.bound = p.bound;
+  ub.key0 = (uint32_t)p.seed; ub.key1 = (uint32_t)(p.seed >> 32); ub.step = (uint32_t)step;
+  for (int l = 1; l <= p.L; ++l) {
+    const LayerPlan &lp = p.layer[l - 1];
+    UpdLayer &u = ub.L[ub.nl++];
+    u.H = reinterpret_cast<int8_t *>(ctx->state + lp.off_h);
+    u.W32 = reinterpret_cast<uint32_t *>(ctx->state + lp.off_w);
+    u.a32 = reinterpret_cast<const uint32_t *>(l == 1 ? d_x : reinterpret_cast<const uint64_t *>(
+                                                               ctx->ws + p.layer[l - 2].off_a));
+    u.kstar = reinterpret_cast<const int16_t *>(ctx->ws + lp.off_kstar);
+    u.P = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p);
+    u.stats = d_stats + 4 * (l - 1);
+    u.ld_h = lp.ld_h; u.nw32 = 2 * lp.words_in; u.words_out = lp.words_out;
+    u.k_in = lp.k_in; u.groups = lp.groups; u.gamma = lp.gamma;
+    const uint64_t T = reinforce_threshold(p_r, lp.k_out);
+    u.t_hi = (uint32_t)(T >> 24); u.t_lo = (uint32_t)(T & 0xFFFFFFu);
+    u.ctr1 = (uint32_t)(l - 1);
+    if (ub.nl == kMaxUpdLayers || l == p.L) {
+      BMLP_TIMED(ctx, BMLP_KERNEL_UPDATE, s, launch_update(ub, s));
+      ub.nl = 0;
+    }
   }
   return BMLP_OK;
 }

@@ -75,7 +75,7 @@ struct LossSelectArgs {
   const int32_t *y; int n;
   int k_out, gamma, groups, thr;
   uint8_t *err, *upd;
-  int16_t *kstar;
+  int16_t *kstar; int ldk; // [groups][ldk]
   int32_t *stats;          // this layer's [4]
 };
 hipError_t launch_loss_select(const LossSelectArgs &a, hipStream_t s);
@@ -84,19 +84,28 @@ hipError_t launch_loss_select(const LossSelectArgs &a, hipStream_t s);
 hipError_t launch_eval_count(const int32_t *yhat, int c, const int32_t *y, int n, int32_t *correct,
                              hipStream_t s);
 
-// Clipped-Perceptron increments + reinforcement + clip + re-sign of one layer.
-struct UpdateArgs {
-  int8_t *H; int ld_h;
-  uint64_t *W; int words_in;
-  const uint64_t *a_prev;
-  const int16_t *kstar; int groups, gamma;
-  const uint64_t *P; int words_out;
-  const int32_t *y; int n, c;
-  int k_in, k_out, bound;
-  uint32_t t_hi, t_lo;     // T_l >> 24 (0..256) and T_l & 0xFFFFFF
-  uint64_t seed; int layer; uint32_t step;
+// Clipped-Perceptron increments + reinforcement + clip + re-sign of up to
+// kMaxUpdLayers layers in one launch.
+struct UpdLayer {
+  int8_t *H;
+  uint32_t *W32;
+  const uint32_t *a32;     // a_{l-1} bit rows as 32-bit words [n][nw32]
+  const int16_t *kstar;    // [groups][ldk]
+  const uint64_t *P;
   int32_t *stats;          // this layer's [4]; reads [1] (|M|), adds [3]
+  int ld_h, nw32, words_out, k_in, groups, gamma;
+  int chunks, block0;      // filled by launch_update
+  uint32_t t_hi, t_lo;     // T_l >> 24 (0..256) and T_l & 0xFFFFFF
+  uint32_t ctr1;           // layer - 1
 };
-hipError_t launch_update(const UpdateArgs &a, hipStream_t s);
+constexpr int kMaxUpdLayers = 8;
+struct UpdateBatch {
+  UpdLayer L[kMaxUpdLayers];
+  int nl;
+  const int32_t *y;
+  int n, ldk, c, bound;
+  uint32_t key0, key1, step;
+};
+hipError_t launch_update(UpdateBatch &b, hipStream_t s);
 
 }  // namespace bmlp

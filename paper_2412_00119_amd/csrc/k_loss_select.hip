@@ -72,7 +72,7 @@ __global__ __launch_bounds__(256) void loss_select_kernel(LossSelectArgs p) {
   const bool err = t.i1 != label;
   const bool upd = err || (t.v1 - t.v2) < p.thr;
   int nsel = 0;
-  int16_t *ks = p.kstar + (size_t)mu * p.groups;
+  int16_t *ks = p.kstar + mu;   // column mu of kstar [groups][ldk]
   if (upd) {
     const int16_t *zr = p.z + (size_t)mu * p.ldz;
     const uint64_t *rho = p.P + (size_t)yl * p.words_out;
@@ -90,11 +90,11 @@ __global__ __launch_bounds__(256) void loss_select_kernel(LossSelectArgs p) {
           best = e;
         }
       }
-      ks[g] = (int16_t)best;
+      ks[(size_t)g * p.ldk] = (int16_t)best;
       nsel += best >= 0;
     }
   } else {
-    for (int g = lane; g < p.groups; g += 64) ks[g] = (int16_t)-1;
+    for (int g = lane; g < p.groups; g += 64) ks[(size_t)g * p.ldk] = (int16_t)-1;
   }
   nsel = wave_sum(nsel);
   if (lane == 0) {
