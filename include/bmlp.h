@@ -56,8 +56,9 @@ enum {
 
 /* Forward GEMM implementation (the binary contraction z = a W^T). */
 enum {
-  BMLP_FWD_AUTO = 0,      /* the library's fastest implementation              */
+  BMLP_FWD_AUTO = 0,      /* the library's fastest implementation (MFMA_FP4)   */
   BMLP_FWD_POPCOUNT = 1,  /* XNOR-popcount over 32-bit words (v_xor + v_bcnt)  */
+  BMLP_FWD_MFMA_FP4 = 2,  /* ±1 as e2m1 operands of the scaled fp4 MFMA: exact  */
 };
 
 /* Limits of this build. */
@@ -105,13 +106,18 @@ typedef struct bmlp_config {
  *   words_in/out     uint64 words per bit row of a_{l-1} / a_l.
  *   ld_h             bytes per row of H_l (>= k_in, a multiple of 64).
  *   robust_thr       ceil(r * K_l), computed in IEEE double.
+ *   ldq_in/out       bytes per fp4 row of K_{l-1} / K_l values (64 per 128 values).
  *   off_h, off_w, off_p  byte offsets in the state buffer of
  *                    H_l  int8   [k_out][ld_h]       hidden weights, perceptron-major
  *                                                    (the transpose of the paper's
  *                                                    K_{l-1} x K_l, so h^k is a row);
  *                                                    bytes past k_in in a row are 0;
  *                    W_l  uint64 [k_out][words_in]   visible weights sign(H_l), bits;
- *                    P_l  uint64 [n_classes][words_out]  fixed classifier, row y is rho^y.
+ *                    P_l  uint64 [n_classes][words_out]  fixed classifier, row y is rho^y;
+ *                    and, as matrix-core operands, copies of W_l (off_wq, uint8
+ *                    [k_out][ldq_in]) and P_l (off_pq, uint8 [n_classes][ldq_out])
+ *                    in fp4 e2m1 (+1 = 0x2, -1 = 0xA, padding 0x0; value k in
+ *                    nibble k & 1 of byte k >> 1).
  *   off_a, off_err, off_upd, off_kstar  byte offsets in the workspace of the
  *                    last train step's
  *                    a_l    uint64 [max_batch][words_out]
@@ -120,13 +126,16 @@ typedef struct bmlp_config {
  *                    kstar_l int16 [groups][max_batch]  easiest wrong
  *                           perceptron of each group as an offset in the
  *                           group; -1 when the group has none or the pattern
- *                           is not in M_l (the pairs of U_l, Algorithm 2).
+ *                           is not in M_l (the pairs of U_l, Algorithm 2)
+ *                    a_l as fp4 (off_aq, uint8 [max_batch][ldq_out]).
  */
 typedef struct bmlp_layer_info {
   int32_t k_in, k_out, gamma, groups;
   int32_t words_in, words_out, ld_h, robust_thr;
   uint64_t off_h, off_w, off_p;
   uint64_t off_a, off_err, off_upd, off_kstar;
+  int32_t ldq_in, ldq_out;
+  uint64_t off_wq, off_pq, off_aq;
 } bmlp_layer_info;
 
 typedef struct bmlp_ctx bmlp_ctx;   /* opaque, host memory only */
@@ -157,7 +166,8 @@ int bmlp_init(const bmlp_config *cfg, void *d_state, void *d_workspace, void *st
               bmlp_ctx **out);
 
 /* Like bmlp_init but keeps H_l and P_l already in d_state (a restored
- * checkpoint) and only recomputes W_l = sign(H_l) from them. */
+ * checkpoint) and only recomputes what derives from them: W_l = sign(H_l)
+ * and the fp4 copies of W_l and P_l. */
 int bmlp_attach(const bmlp_config *cfg, void *d_state, void *d_workspace, void *stream,
                 bmlp_ctx **out);
 

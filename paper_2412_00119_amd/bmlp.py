@@ -26,6 +26,7 @@ BMLP_ESTATE = -4
 
 BMLP_FWD_AUTO = 0
 BMLP_FWD_POPCOUNT = 1
+BMLP_FWD_MFMA_FP4 = 2
 
 MAX_BATCH = 16384
 
@@ -58,7 +59,9 @@ class bmlp_layer_info(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("k_in", "k_out", "gamma", "groups", "words_in", "words_out", "ld_h", "robust_thr")] + \
                [(n, ctypes.c_uint64) for n in
-                ("off_h", "off_w", "off_p", "off_a", "off_err", "off_upd", "off_kstar")]
+                ("off_h", "off_w", "off_p", "off_a", "off_err", "off_upd", "off_kstar")] + \
+               [(n, ctypes.c_int32) for n in ("ldq_in", "ldq_out")] + \
+               [(n, ctypes.c_uint64) for n in ("off_wq", "off_pq", "off_aq")]
 
 
 _lib = None
@@ -318,6 +321,16 @@ class BMLP:
         i = self.info[l - 1]
         return self._view(self.state, i.off_p, self.n_classes * i.words_out * 8, self.torch.int64,
                           (self.n_classes, i.words_out))
+
+    def Wq(self, l: int):
+        """W_l as fp4 operand rows, uint8 [K_l][ldq_in]."""
+        i = self.info[l - 1]
+        return self._view(self.state, i.off_wq, i.k_out * i.ldq_in, self.torch.uint8, (i.k_out, i.ldq_in))
+
+    def Pq(self, l: int):
+        i = self.info[l - 1]
+        return self._view(self.state, i.off_pq, self.n_classes * i.ldq_out, self.torch.uint8,
+                          (self.n_classes, i.ldq_out))
 
     def trace(self, l: int, n: int):
         """Last train step's a_l bits, err, upd and kstar of layer l (first n patterns)."""

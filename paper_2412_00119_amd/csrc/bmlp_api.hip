@@ -8,6 +8,7 @@
 #include <vector>
 
 #include "bmlp_internal.h"
+#include "fp4.h"
 
 struct ProfRec {
   int kind;
@@ -84,7 +85,9 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
   if (cfg->bound < 1 || cfg->bound > 127 || (cfg->bound & 1) == 0) return BMLP_EINVAL;
   if (cfg->group_size < 0 || cfg->group_size > BMLP_MAX_GROUP) return BMLP_ESHAPE;
   if (!(cfg->robustness >= 0.0) || !isfinite(cfg->robustness)) return BMLP_EINVAL;
-  if (cfg->fwd_impl != BMLP_FWD_AUTO && cfg->fwd_impl != BMLP_FWD_POPCOUNT) return BMLP_EINVAL;
+  if (cfg->fwd_impl != BMLP_FWD_AUTO && cfg->fwd_impl != BMLP_FWD_POPCOUNT &&
+      cfg->fwd_impl != BMLP_FWD_MFMA_FP4)
+    return BMLP_EINVAL;
   memset(p, 0, sizeof(*p));
   p->L = cfg->n_layers;
   p->c = cfg->n_classes;
@@ -112,6 +115,8 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
     lp.words_in = words64(lp.k_in);
     lp.words_out = words64(lp.k_out);
     lp.ld_h = 64 * lp.words_in;
+    lp.ldq_in = fp4_row_bytes(lp.k_in);
+    lp.ldq_out = fp4_row_bytes(lp.k_out);
     const double thr = ceil(p->r * (double)lp.k_out);
     if (thr > 2147483647.0) return BMLP_EINVAL;
     lp.robust_thr = (int)thr;
@@ -121,6 +126,10 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
     so = align256(so + (size_t)lp.k_out * lp.words_in * 8);
     lp.off_p = so;
     so = align256(so + (size_t)p->c * lp.words_out * 8);
+    lp.off_wq = so;
+    so = align256(so + (size_t)lp.k_out * lp.ldq_in);
+    lp.off_pq = so;
+    so = align256(so + (size_t)p->c * lp.ldq_out);
   }
   p->state_bytes = so;
   size_t wo = 0;
@@ -134,7 +143,12 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
     wo = align256(wo + (size_t)nb);
     lp.off_kstar = wo;
     wo = align256(wo + (size_t)nb * lp.groups * 2);
+    lp.off_aq = wo;
+    wo = align256(wo + (size_t)nb * lp.ldq_out);
   }
+  p->ldq0 = fp4_row_bytes(p->widths[0]);
+  p->off_xq = wo;
+  wo = align256(wo + (size_t)nb * p->ldq0);
   p->ldz = 64 * words64(kmax);
   p->off_z = wo;
   wo = align256(wo + (size_t)nb * p->ldz * 2);
@@ -158,11 +172,41 @@ uint64_t reinforce_threshold(double p_r, int k) {
   return (uint64_t)t;
 }
 
+bool use_mfma(const Plan &p) { return p.fwd_impl != BMLP_FWD_POPCOUNT; }
+
+// Forward of every layer for inference (y_hat out) or evaluation (counts).
 int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32_t *yhat_out,
                    const int32_t *y, int32_t *correct) {
   const Plan &p = ctx->plan;
-  const uint64_t *a_prev = x;
   int32_t *yh_ws = reinterpret_cast<int32_t *>(ctx->ws + p.off_yhat);
+  if (use_mfma(p)) {
+    uint8_t *xq = ctx->ws + p.off_xq;
+    BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s,
+               launch_fp4_rows(x, p.layer[0].words_in, p.widths[0], n, xq, p.ldq0, nullptr, 0, s));
+    const uint8_t *aq_prev = xq;
+    for (int l = 1; l <= p.L; ++l) {
+      const LayerPlan &lp = p.layer[l - 1];
+      FwdArgs f{};
+      f.A = aq_prev; f.lda = lp.ldq_in;
+      f.B = ctx->state + lp.off_wq; f.ldb = lp.ldq_in;
+      f.M = n; f.N = lp.k_out; f.ksteps = lp.ldq_in / 64;
+      f.abits = reinterpret_cast<uint64_t *>(ctx->ws + lp.off_a); f.words_out = lp.words_out;
+      f.afp4 = ctx->ws + lp.off_aq; f.ld_af = lp.ldq_out;
+      f.mode = kFwdPlain;
+      BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s, launch_fwd_fp4(f, s));
+      ClsArgs c{};
+      c.A = f.afp4; c.lda = lp.ldq_out;
+      c.P = ctx->state + lp.off_pq; c.ldp = lp.ldq_out;
+      c.n = n; c.c = p.c; c.ksteps = lp.ldq_out / 64;
+      c.yhat = yhat_out ? yhat_out + (size_t)(l - 1) * n * p.c : yh_ws; c.ldo = p.c;
+      c.mode = correct ? kClsEval : kClsYhatOnly;
+      c.y = y; c.correct = correct ? correct + (l - 1) : nullptr;
+      BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_cls_fp4(c, s));
+      aq_prev = f.afp4;
+    }
+    return BMLP_OK;
+  }
+  const uint64_t *a_prev = x;
   for (int l = 1; l <= p.L; ++l) {
     const LayerPlan &lp = p.layer[l - 1];
     const uint64_t *W = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_w);
@@ -211,6 +255,11 @@ int setup(const bmlp_config *cfg, void *d_state, void *d_ws, void *stream, bmlp_
     uint64_t *P = reinterpret_cast<uint64_t *>(ctx->state + lp.off_p);
     hipError_t e = launch_init_h(H, lp.ld_h, W, lp.words_in, lp.k_in, lp.k_out, p.seed, l, from_h, s);
     if (e == hipSuccess && !from_h) e = launch_init_p(P, lp.words_out, lp.k_out, p.c, p.seed, l, s);
+    // fp4 operand copies of W_l and P_l for the matrix-core path
+    if (e == hipSuccess)
+      e = launch_fp4_rows(W, lp.words_in, lp.k_in, lp.k_out, ctx->state + lp.off_wq, lp.ldq_in, nullptr, 0, s);
+    if (e == hipSuccess)
+      e = launch_fp4_rows(P, lp.words_out, lp.k_out, p.c, ctx->state + lp.off_pq, lp.ldq_out, nullptr, 0, s);
     if (e != hipSuccess) {
       delete ctx;
       return hip_fail(e, "init");
@@ -259,6 +308,11 @@ int bmlp_describe(const bmlp_config *cfg, int32_t l, bmlp_layer_info *info) {
   info->off_err = lp.off_err;
   info->off_upd = lp.off_upd;
   info->off_kstar = lp.off_kstar;
+  info->ldq_in = lp.ldq_in;
+  info->ldq_out = lp.ldq_out;
+  info->off_wq = lp.off_wq;
+  info->off_pq = lp.off_pq;
+  info->off_aq = lp.off_aq;
   return BMLP_OK;
 }
 
@@ -309,37 +363,74 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
   if (!(p_r >= 0.0) || !isfinite(p_r)) return BMLP_EINVAL;
   const Plan &p = ctx->plan;
   hipStream_t s = as_stream(stream);
-  BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s, launch_fill_i32(d_stats, 4 * p.L, 0, s));
+  const bool mfma = use_mfma(p);
+  if (n == 0 || !mfma)
+    BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s, launch_fill_i32(d_stats, 4 * p.L, 0, s));
   if (n == 0) return BMLP_OK;
-  const uint64_t *a_prev = d_x;
   int16_t *z = reinterpret_cast<int16_t *>(ctx->ws + p.off_z);
   int32_t *yh = reinterpret_cast<int32_t *>(ctx->ws + p.off_yhat);
+  uint8_t *xq = ctx->ws + p.off_xq;
+  if (mfma)   // input as fp4 rows; also zeroes the statistics
+    BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s,
+               launch_fp4_rows(d_x, p.layer[0].words_in, p.widths[0], n, xq, p.ldq0, d_stats, 4 * p.L, s));
+  const uint64_t *a_prev = d_x;
+  const uint8_t *aq_prev = xq;
   for (int l = 1; l <= p.L; ++l) {
     const LayerPlan &lp = p.layer[l - 1];
-    int8_t *H = reinterpret_cast<int8_t *>(ctx->state + lp.off_h);
-    uint64_t *W = reinterpret_cast<uint64_t *>(ctx->state + lp.off_w);
+    const uint64_t *W = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_w);
     const uint64_t *P = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p);
     uint64_t *a = reinterpret_cast<uint64_t *>(ctx->ws + lp.off_a);
     uint8_t *err = ctx->ws + lp.off_err;
     uint8_t *upd = ctx->ws + lp.off_upd;
     int16_t *kstar = reinterpret_cast<int16_t *>(ctx->ws + lp.off_kstar);
     int32_t *stats = d_stats + 4 * (l - 1);
-
-    // Algorithm 1: z_l, a_l, y_hat_l
-    BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s,
-               launch_fwd_popcount(a_prev, lp.words_in, lp.k_in, W, n, lp.k_out, z, p.ldz, a,
-                                   lp.words_out, s));
-    BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s, launch_fill_i32(yh, n * p.c, lp.k_out, s));
-    BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_cls_popcount(a, lp.words_out, lp.k_out, P, n, p.c, yh, p.c, s));
-    // Eq. 1, robustness, M_l; Algorithm 2
     LossSelectArgs ls{};
-    ls.yhat = yh; ls.c = p.c;
+    ls.c = p.c;
     ls.z = z; ls.ldz = p.ldz;
     ls.P = P; ls.words_out = lp.words_out;
     ls.y = d_y; ls.n = n;
     ls.k_out = lp.k_out; ls.gamma = lp.gamma; ls.groups = lp.groups; ls.thr = lp.robust_thr;
     ls.err = err; ls.upd = upd; ls.kstar = kstar; ls.ldk = p.max_batch; ls.stats = stats;
-    BMLP_TIMED(ctx, BMLP_KERNEL_SELECT, s, launch_loss_select(ls, s));
+    if (mfma) {
+      const bool fused = lp.gamma == 64;
+      // Algorithm 1 lines 8-9 (+ Algorithm 2 when fused)
+      FwdArgs f{};
+      f.A = aq_prev; f.lda = lp.ldq_in;
+      f.B = ctx->state + lp.off_wq; f.ldb = lp.ldq_in;
+      f.M = n; f.N = lp.k_out; f.ksteps = lp.ldq_in / 64;
+      f.abits = a; f.words_out = lp.words_out;
+      f.afp4 = ctx->ws + lp.off_aq; f.ld_af = lp.ldq_out;
+      f.mode = fused ? kFwdFusedSelect : kFwdWriteZ;
+      f.kstar = kstar; f.ldk = p.max_batch;
+      f.y = d_y; f.Pbits = P; f.c = p.c;
+      f.z = z; f.ldz = p.ldz;
+      BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s, launch_fwd_fp4(f, s));
+      // Algorithm 1 lines 10-15
+      ClsArgs c{};
+      c.A = f.afp4; c.lda = lp.ldq_out;
+      c.P = ctx->state + lp.off_pq; c.ldp = lp.ldq_out;
+      c.n = n; c.c = p.c; c.ksteps = lp.ldq_out / 64;
+      c.yhat = yh; c.ldo = p.c;
+      c.mode = kClsTrain;
+      c.y = d_y; c.thr = lp.robust_thr;
+      c.err = err; c.upd = upd;
+      c.kstar = fused ? kstar : nullptr; c.ldk = p.max_batch; c.groups = lp.groups;
+      c.stats = stats;
+      BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_cls_fp4(c, s));
+      if (!fused) {   // Algorithm 2 from the stored z
+        ls.yhat = nullptr;
+        BMLP_TIMED(ctx, BMLP_KERNEL_SELECT, s, launch_loss_select(ls, s));
+      }
+      aq_prev = f.afp4;
+    } else {
+      BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s,
+                 launch_fwd_popcount(a_prev, lp.words_in, lp.k_in, W, n, lp.k_out, z, p.ldz, a,
+                                     lp.words_out, s));
+      BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s, launch_fill_i32(yh, n * p.c, lp.k_out, s));
+      BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_cls_popcount(a, lp.words_out, lp.k_out, P, n, p.c, yh, p.c, s));
+      ls.yhat = yh;
+      BMLP_TIMED(ctx, BMLP_KERNEL_SELECT, s, launch_loss_select(ls, s));
+    }
     a_prev = a;
   }
   // Algorithm 3 for every layer (each layer's forward above used its
@@ -352,6 +443,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
     UpdLayer &u = ub.L[ub.nl++];
     u.H = reinterpret_cast<int8_t *>(ctx->state + lp.off_h);
     u.W32 = reinterpret_cast<uint32_t *>(ctx->state + lp.off_w);
+    u.Wq = ctx->state + lp.off_wq; u.ldq = lp.ldq_in;
     u.a32 = reinterpret_cast<const uint32_t *>(l == 1 ? d_x : reinterpret_cast<const uint64_t *>(
                                                                ctx->ws + p.layer[l - 2].off_a));
     u.kstar = reinterpret_cast<const int16_t *>(ctx->ws + lp.off_kstar);

@@ -22,8 +22,9 @@ struct LayerPlan {
   int words_in, words_out;   // uint64 words per bit row of a_{l-1} / a_l
   int ld_h;                  // bytes per H row, multiple of 64
   int robust_thr;            // ceil(r K_l)
-  size_t off_h, off_w, off_p;
-  size_t off_a, off_err, off_upd, off_kstar;
+  int ldq_in, ldq_out;       // bytes per fp4 row of K_{l-1} / K_l elements
+  size_t off_h, off_w, off_p, off_wq, off_pq;     // state
+  size_t off_a, off_err, off_upd, off_kstar, off_aq;   // workspace
 };
 
 struct Plan {
@@ -33,7 +34,8 @@ struct Plan {
   int widths[BMLP_MAX_LAYERS + 1];
   LayerPlan layer[BMLP_MAX_LAYERS];   // layer[l-1] describes layer l
   int ldz;                            // int16 elements per row of the z scratch
-  size_t off_z, off_yhat;             // shared scratch in the workspace
+  int ldq0;                           // bytes per fp4 row of the input
+  size_t off_z, off_yhat, off_xq;     // shared scratch in the workspace
   size_t state_bytes, ws_bytes;
 };
 
@@ -67,7 +69,44 @@ hipError_t launch_fwd_popcount(const uint64_t *a_prev, int words_in, int k_in, c
 hipError_t launch_cls_popcount(const uint64_t *a, int words, int k, const uint64_t *P, int n,
                                int c, int32_t *out, int ldo, hipStream_t s);
 
-// 01-loss, margin, M and the easiest wrong perceptron per group.
+// Forward on the matrix cores with fp4 operands.
+enum { kFwdFusedSelect = 0, kFwdWriteZ = 1, kFwdPlain = 2 };
+struct FwdArgs {
+  const uint8_t *A; int lda;        // a_{l-1} fp4 [M][lda]
+  const uint8_t *B; int ldb;        // W_l fp4 [N][ldb]
+  int M, N, ksteps;                 // ksteps = lda / 64
+  uint64_t *abits; int words_out;   // a_l bits [M][words_out]
+  uint8_t *afp4; int ld_af;         // a_l fp4 [M][ld_af]
+  int mode;
+  int16_t *kstar; int ldk;          // kFwdFusedSelect (gamma = 64): raw selection [groups][ldk]
+  const int32_t *y; const uint64_t *Pbits; int c;
+  int16_t *z; int ldz;              // kFwdWriteZ
+  int nt_m, nt_n, xcd_remap;        // set by the launcher
+};
+hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s);
+
+// bit rows [R][words] of K columns -> fp4 rows [R][ldq]; also zeroes zero[0..nzero)
+hipError_t launch_fp4_rows(const uint64_t *bits, int words, int K, int R, uint8_t *q, int ldq,
+                           int32_t *zero, int nzero, hipStream_t s);
+
+// Classifier on the matrix cores, then the local error signal.
+enum { kClsTrain = 0, kClsYhatOnly = 1, kClsEval = 2 };
+struct ClsArgs {
+  const uint8_t *A; int lda;        // a_l fp4 [n][lda]
+  const uint8_t *P; int ldp;        // P_l fp4 [c][ldp]
+  int n, c, ksteps;
+  int32_t *yhat; int ldo;           // y_hat int32 [n][ldo]
+  int mode;
+  const int32_t *y; int thr;
+  uint8_t *err, *upd;
+  int16_t *kstar; int ldk, groups;  // train: masks patterns outside M (may be null)
+  int32_t *stats;                   // train: this layer's [4]
+  int32_t *correct;                 // eval
+};
+hipError_t launch_cls_fp4(const ClsArgs &a, hipStream_t s);
+
+// 01-loss, margin, M and the easiest wrong perceptron per group.  With
+// yhat == nullptr the kernel only selects, for the patterns whose upd is set.
 struct LossSelectArgs {
   const int32_t *yhat; int c;
   const int16_t *z; int ldz;
@@ -89,6 +128,7 @@ hipError_t launch_eval_count(const int32_t *yhat, int c, const int32_t *y, int n
 struct UpdLayer {
   int8_t *H;
   uint32_t *W32;
+  uint8_t *Wq; int ldq;    // W_l as fp4 [K_l][ldq]
   const uint32_t *a32;     // a_{l-1} bit rows as 32-bit words [n][nw32]
   const int16_t *kstar;    // [groups][ldk]
   const uint64_t *P;

@@ -66,11 +66,17 @@ __global__ __launch_bounds__(256) void loss_select_kernel(LossSelectArgs p) {
   const int mu = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (mu >= p.n) return;
-  const Top2 t = wave_top2(p.yhat + (size_t)mu * p.c, p.c, lane);
+  const bool select_only = p.yhat == nullptr;   // upd already computed
   const int label = p.y[mu];
   const int yl = min(max(label, 0), p.c - 1);      // stay inside P on a bad label
-  const bool err = t.i1 != label;
-  const bool upd = err || (t.v1 - t.v2) < p.thr;
+  bool err = false, upd;
+  if (select_only) {
+    upd = p.upd[mu] != 0;
+  } else {
+    const Top2 t = wave_top2(p.yhat + (size_t)mu * p.c, p.c, lane);
+    err = t.i1 != label;
+    upd = err || (t.v1 - t.v2) < p.thr;
+  }
   int nsel = 0;
   int16_t *ks = p.kstar + mu;   // column mu of kstar [groups][ldk]
   if (upd) {
@@ -98,10 +104,12 @@ __global__ __launch_bounds__(256) void loss_select_kernel(LossSelectArgs p) {
   }
   nsel = wave_sum(nsel);
   if (lane == 0) {
-    p.err[mu] = err ? 1 : 0;
-    p.upd[mu] = upd ? 1 : 0;
-    if (err) atomicAdd(p.stats + 0, 1);
-    if (upd) atomicAdd(p.stats + 1, 1);
+    if (!select_only) {
+      p.err[mu] = err ? 1 : 0;
+      p.upd[mu] = upd ? 1 : 0;
+      if (err) atomicAdd(p.stats + 0, 1);
+      if (upd) atomicAdd(p.stats + 1, 1);
+    }
     if (nsel) atomicAdd(p.stats + 2, nsel);
   }
 }

@@ -19,6 +19,7 @@
 // packed 16-bit lanes: with cnt_i the count, sum_i = 2 cnt_i - S and
 // dH_i = 4 cnt_i - 2 S.  No two work-groups write the same bytes of H or W.
 #include "bmlp_internal.h"
+#include "fp4.h"
 #include "philox.h"
 
 namespace bmlp {
@@ -316,6 +317,12 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     reinterpret_cast<uint4 *>(hrow)[0] = make_uint4(hw[0], hw[1], hw[2], hw[3]);
     reinterpret_cast<uint4 *>(hrow)[1] = make_uint4(hw[4], hw[5], hw[6], hw[7]);
     U.W32[(size_t)k * U.nw32 + cw] = wbits;
+    {
+      uint32_t o[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[q] = fp4_from_bits8(wbits >> (8 * q), validmask >> (8 * q));
+      *reinterpret_cast<uint4 *>(U.Wq + (size_t)k * U.ldq + cw * 16) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
   }
 
   nreinf = wave_sum(nreinf);

@@ -48,11 +48,15 @@ CASES = [
 ]
 
 
+IMPLS = {"popcount": 1, "mfma_fp4": 2}
+
+
+@pytest.mark.parametrize("impl", list(IMPLS))
 @pytest.mark.parametrize("case", CASES, ids=[f"{c[0]}-c{c[1]}-B{c[2]}-g{c[3]}-n{c[4]}" for c in CASES])
-def test_random_shapes(case):
+def test_random_shapes(case, impl):
     widths, c, bound, gamma, n, steps, p_r, r = case
     rng = np.random.default_rng(sum(widths) + n)
-    p = Pair(widths, c, bound, n + 3, gamma, r, seed=int(rng.integers(1 << 62)))
+    p = Pair(widths, c, bound, n + 3, gamma, r, seed=int(rng.integers(1 << 62)), fwd_impl=IMPLS[impl])
     for t in range(steps):
         note(f"shape {widths} step {t}")
         x = random_pm1((n, widths[0]), rng)
@@ -60,9 +64,10 @@ def test_random_shapes(case):
         p.step(x, y, 1000 + t, p_r, tag=f"step {t}")
 
 
-def _workload_run(w, steps, n=None, check_every=1):
+def _workload_run(w, steps, n=None, check_every=1, fwd_impl=0):
     n = w.batch if n is None else n
-    p = Pair(w.widths, w.n_classes, w.bound, w.batch, w.group_size, w.robustness, w.seed_model)
+    p = Pair(w.widths, w.n_classes, w.bound, w.batch, w.group_size, w.robustness, w.seed_model,
+             fwd_impl=fwd_impl)
     d = synth.make_split(w, "train", n=steps * n)
     for t, (x, y) in enumerate(d.batches(n)):
         if t >= steps:
@@ -72,13 +77,15 @@ def _workload_run(w, steps, n=None, check_every=1):
     return p
 
 
-def test_tiny_workload_full_epoch():
+@pytest.mark.parametrize("impl", list(IMPLS))
+def test_tiny_workload_full_epoch(impl):
     w = synth.TINY
-    _workload_run(w, w.steps_per_epoch)
+    _workload_run(w, w.steps_per_epoch, fwd_impl=IMPLS[impl])
 
 
-def test_small_workload():
-    _workload_run(synth.SMALL, 4)
+@pytest.mark.parametrize("impl", list(IMPLS))
+def test_small_workload(impl):
+    _workload_run(synth.SMALL, 4, fwd_impl=IMPLS[impl])
 
 
 def test_field_workload():
@@ -89,10 +96,12 @@ def test_headline_workload_two_steps():
     _workload_run(synth.HEADLINE, 2)
 
 
-def test_forward_and_eval_match():
+@pytest.mark.parametrize("impl", list(IMPLS))
+def test_forward_and_eval_match(impl):
     torch = torch_cuda()
     w = synth.SMALL
-    p = Pair(w.widths, w.n_classes, w.bound, 300, w.group_size, w.robustness, w.seed_model)
+    p = Pair(w.widths, w.n_classes, w.bound, 300, w.group_size, w.robustness, w.seed_model,
+             fwd_impl=IMPLS[impl])
     d = synth.make_split(w, "train", n=512)
     for t, (x, y) in enumerate(d.batches(256)):
         p.step(x, y, t, w.p_r, check_state=False)
