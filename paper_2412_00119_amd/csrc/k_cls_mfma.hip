@@ -2,10 +2,15 @@
 // y_hat = a_l P_l^T, the 01-loss of Eq. 1 and the robustness test that
 // builds M_l).
 //
-// A work-group owns 16 patterns and all classes: each wave takes every
-// fourth block of 16 classes (at most 1024 classes per pass), walks K in
-// steps of 128 fp4 elements with v_mfma_scale_f32_16x16x128_f8f6f4 and
-// writes y_hat as int32.  After a barrier each wave takes four of the
+// A work-group owns 16 patterns and all classes, taken CB blocks of 16
+// classes per pass (CB is a template parameter sized to the class count).
+// The four waves split K (wave w takes K steps w, w+4, ...), each keeping
+// one 16x16 accumulator per block of 16 classes, and prefetch the next K
+// step's operands while the current one runs on the matrix cores; loads are
+// unconditional (indices clamped, data masked) so the prefetch is not
+// serialised by conservative waits.  The
+// partial sums are exact integers, so adding them in LDS with float atomics
+// gives the same y_hat in any order.  After a barrier each wave takes four of the
 // patterns: first argmax (lowest class on ties), the two largest values
 // (tau = top1 - top2, 0 on a tie), err = (pred != y), upd = err or
 // tau < ceil(r K_l).  Patterns outside M_l get no selected perceptron
@@ -21,7 +26,6 @@ namespace {
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
-constexpr int CPW = 16;   // class blocks per wave per pass -> 4 * 16 * 16 = 1024 classes
 
 __device__ __forceinline__ v4f mfma_fp4(const uint4 &a, const uint4 &b, v4f c) {
   const v8i av = {(int)a.x, (int)a.y, (int)a.z, (int)a.w, 0, 0, 0, 0};
@@ -52,46 +56,70 @@ __device__ __forceinline__ int wave_sum(int v) {
   return v;
 }
 
+template <int CB>
 __global__ __launch_bounds__(256) void cls_fp4_kernel(ClsArgs p) {
+  __shared__ float red[16][CB * 16];
+  __shared__ int cnt[4];   // block totals of err, upd, selected, correct
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int m0 = blockIdx.x * 16;
   const int lr = lane & 15, lk = (lane >> 4) * 16;
   const int nblk = (p.c + 15) / 16;
   const int am = m0 + lr;
-  const uint8_t *arow = am < p.n ? p.A + (size_t)am * p.lda : nullptr;
+  const uint32_t amask = am < p.n ? 0xFFFFFFFFu : 0u;
+  const uint8_t *arow = p.A + (size_t)min(am, p.n - 1) * p.lda + lk;
+  auto masked = [](const uint4 &v, uint32_t m) { return make_uint4(v.x & m, v.y & m, v.z & m, v.w & m); };
 
-  for (int cb0 = 0; cb0 < nblk; cb0 += 4 * CPW) {
-    v4f acc[CPW];
+  for (int cb0 = 0; cb0 < nblk; cb0 += CB) {
+    const int nb = min(CB, nblk - cb0);
+    for (int i = tid; i < 16 * CB * 16; i += 256) (&red[0][0])[i] = 0.f;
+    v4f acc[CB];
 #pragma unroll
-    for (int j = 0; j < CPW; ++j) acc[j] = (v4f){0.f, 0.f, 0.f, 0.f};
-    for (int ks = 0; ks < p.ksteps; ++ks) {
-      const uint4 a = arow ? *reinterpret_cast<const uint4 *>(arow + ks * 64 + lk) : make_uint4(0, 0, 0, 0);
+    for (int j = 0; j < CB; ++j) acc[j] = (v4f){0.f, 0.f, 0.f, 0.f};
+    const uint8_t *brow[CB];
+    uint32_t bmask[CB];
 #pragma unroll
-      for (int j = 0; j < CPW; ++j) {
-        const int cb = cb0 + wave + 4 * j;
-        if (cb < nblk) {   // uniform per wave
-          const int cls = cb * 16 + lr;
-          const uint4 b = cls < p.c ? *reinterpret_cast<const uint4 *>(p.P + (size_t)cls * p.ldp + ks * 64 + lk)
-                                    : make_uint4(0, 0, 0, 0);
-          acc[j] = mfma_fp4(a, b, acc[j]);
-        }
-      }
+    for (int j = 0; j < CB; ++j) {
+      const int cls = (cb0 + j) * 16 + lr;
+      bmask[j] = cls < p.c ? 0xFFFFFFFFu : 0u;
+      brow[j] = p.P + (size_t)min(cls, p.c - 1) * p.ldp + lk;
     }
-    // y_hat: lane holds class cb*16 + (lane & 15), patterns m0 + 4*(lane >> 4) + e
+    uint4 a_cur, b_cur[CB], a_nxt, b_nxt[CB];
+    auto load = [&](uint4 &a, uint4 (&b)[CB], int ks) {
+      a = *reinterpret_cast<const uint4 *>(arow + ks * 64);
 #pragma unroll
-    for (int j = 0; j < CPW; ++j) {
-      const int cb = cb0 + wave + 4 * j;
-      if (cb < nblk) {
-        const int cls = cb * 16 + lr;
+      for (int j = 0; j < CB; ++j) b[j] = *reinterpret_cast<const uint4 *>(brow[j] + ks * 64);
+    };
+    int ks = wave;
+    if (ks < p.ksteps) load(a_cur, b_cur, ks);
+    while (ks < p.ksteps) {
+      const int kn = ks + 4;
+      if (kn < p.ksteps) load(a_nxt, b_nxt, kn);
+      const uint4 am4 = masked(a_cur, amask);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int m = m0 + 4 * (lane >> 4) + e;
-          if (m < p.n && cls < p.c) p.yhat[(size_t)m * p.ldo + cls] = (int32_t)acc[j][e];
-        }
-      }
+      for (int j = 0; j < CB; ++j)
+        if (j < nb) acc[j] = mfma_fp4(am4, masked(b_cur[j], bmask[j]), acc[j]);
+      a_cur = a_nxt;
+#pragma unroll
+      for (int j = 0; j < CB; ++j) b_cur[j] = b_nxt[j];
+      ks = kn;
     }
+    __syncthreads();   // red is zeroed
+    // lane holds classes (cb0 + j)*16 + (lane & 15) of patterns 4*(lane >> 4) + e
+#pragma unroll
+    for (int j = 0; j < CB; ++j)
+      if (j < nb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) atomicAdd(&red[4 * (lane >> 4) + e][j * 16 + lr], acc[j][e]);
+    __syncthreads();
+    for (int i = tid; i < 16 * CB * 16; i += 256) {
+      const int r = i / (CB * 16), cl = i % (CB * 16);
+      const int m = m0 + r, cls = cb0 * 16 + cl;
+      if (m < p.n && cls < p.c) p.yhat[(size_t)m * p.ldo + cls] = (int32_t)red[r][cl];
+    }
+    __syncthreads();
   }
   if (p.mode == kClsYhatOnly) return;
+  if (tid < 4) cnt[tid] = 0;
   __syncthreads();   // y_hat of the 16 patterns is complete (global writes, same work-group)
 
   for (int r = wave; r < 16; r += 4) {
@@ -119,7 +147,7 @@ __global__ __launch_bounds__(256) void cls_fp4_kernel(ClsArgs p) {
     }
     const int label = p.y[mu];
     if (p.mode == kClsEval) {
-      if (lane == 0 && t.i1 == label) atomicAdd(p.correct, 1);
+      if (lane == 0 && t.i1 == label) atomicAdd(&cnt[3], 1);
       continue;
     }
     const bool err = t.i1 != label;
@@ -138,9 +166,21 @@ __global__ __launch_bounds__(256) void cls_fp4_kernel(ClsArgs p) {
     if (lane == 0) {
       p.err[mu] = err ? 1 : 0;
       p.upd[mu] = upd ? 1 : 0;
-      if (err) atomicAdd(p.stats + 0, 1);
-      if (upd) atomicAdd(p.stats + 1, 1);
-      if (nsel) atomicAdd(p.stats + 2, nsel);
+      if (err) atomicAdd(&cnt[0], 1);
+      if (upd) atomicAdd(&cnt[1], 1);
+      if (nsel) atomicAdd(&cnt[2], nsel);
+    }
+  }
+  // one global atomic per counter and work-group: same-address atomics from
+  // every pattern would serialise in L2
+  __syncthreads();
+  if (tid == 0) {
+    if (p.mode == kClsEval) {
+      if (cnt[3]) atomicAdd(p.correct, cnt[3]);
+    } else {
+      if (cnt[0]) atomicAdd(p.stats + 0, cnt[0]);
+      if (cnt[1]) atomicAdd(p.stats + 1, cnt[1]);
+      if (cnt[2]) atomicAdd(p.stats + 2, cnt[2]);
     }
   }
 }
@@ -149,7 +189,18 @@ __global__ __launch_bounds__(256) void cls_fp4_kernel(ClsArgs p) {
 
 hipError_t launch_cls_fp4(const ClsArgs &a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(cls_fp4_kernel, dim3((a.n + 15) / 16), dim3(256), 0, s, a);
+  const int nblk = (a.c + 15) / 16;
+  const dim3 grid((a.n + 15) / 16), block(256);
+  if (nblk <= 1)
+    hipLaunchKernelGGL(cls_fp4_kernel<1>, grid, block, 0, s, a);
+  else if (nblk <= 2)
+    hipLaunchKernelGGL(cls_fp4_kernel<2>, grid, block, 0, s, a);
+  else if (nblk <= 4)
+    hipLaunchKernelGGL(cls_fp4_kernel<4>, grid, block, 0, s, a);
+  else if (nblk <= 8)
+    hipLaunchKernelGGL(cls_fp4_kernel<8>, grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL(cls_fp4_kernel<16>, grid, block, 0, s, a);
   return hipGetLastError();
 }
 

@@ -3,15 +3,21 @@
 // the epilogue.
 //
 // Both operands are ±1 matrices stored as fp4 (see fp4.h), so z is computed
-// exactly by v_mfma_scale_f32_16x16x128_f8f6f4 with fp32 accumulation.  A
+// exactly by v_mfma_scale_f32_32x32x64_f8f6f4 with fp32 accumulation (on
+// gfx950 the 32x32x64 shape runs fp4 at twice the rate of 16x16x128).  A
 // work-group computes a 128 x 128 tile of z (patterns x perceptrons) with
-// four waves of 64 x 64; K is walked in steps of 128 elements through
-// double-buffered LDS tiles.  The epilogue never writes z to memory:
+// four waves of 64 x 64; K is walked in steps of 128 elements through a
+// ring of kStages LDS buffers filled by direct-to-LDS loads
+// (global_load_lds_dwordx4), kStages - 1 steps ahead of the matrix cores, with
+// one barrier per step.  Rows past the matrix end are clamped into range:
+// they only feed outputs that are never stored.  The epilogue never writes z
+// to memory:
 //   * a_l as bit rows (wave ballots) and as fp4 rows for the next layer and
 //     the classifier;
 //   * for gamma = 64, the easiest wrong perceptron of each group: among the
 //     columns k of the group with delta_k = z_k rho^{y}_k < 0, the smallest
-//     |z_k|, lowest k on ties (key = |z| << 8 | k, min-reduced across lanes);
+//     |z_k|, lowest k on ties (key = |z| << 8 | k, min-reduced across lanes
+//     with a butterfly reduce-scatter, so each lane ends with one row);
 //   * for any other gamma, z as int16 for the generic selection kernel.
 // Work-groups are mapped so that each XCD (work-group id mod 8) works on
 // its own slice of W_l, which then stays in that XCD's L2.
@@ -22,22 +28,47 @@ namespace bmlp {
 namespace {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
-typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v16f __attribute__((ext_vector_type(16)));
 
 constexpr int TM = 128, TN = 128;   // tile of z
 constexpr int KB = 64;              // bytes per row per K step (128 fp4)
+constexpr int kStages = 4;          // LDS ring depth
 
-__device__ __forceinline__ v4f mfma_fp4(const uint4 &a, const uint4 &b, v4f c) {
+typedef __attribute__((address_space(3))) void lds_void;
+
+// 16 bytes per lane from global memory to LDS at dst + 16 * lane
+__device__ __forceinline__ void dma16(const void *src, void *dst_wave_base) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void *)dst_wave_base, 16, 0, 0);
+}
+
+// wait until at most n vector-memory operations of this wave are outstanding
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0xF70 | N);   // expcnt and lgkmcnt left unconstrained
+}
+
+// XOR swizzle of the 16-byte chunk index within a 64-byte LDS row
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+
+// lane l: A row / B column (l & 31), K elements 32*(l >> 5) .. +32 of the
+// 64-element step; result element i of lane l is row 8*(i>>2) + 4*(l>>5) + (i&3),
+// column (l & 31)
+__device__ __forceinline__ v16f mfma_fp4(const uint4 &a, const uint4 &b, v16f c) {
   const v8i av = {(int)a.x, (int)a.y, (int)a.z, (int)a.w, 0, 0, 0, 0};
   const v8i bv = {(int)b.x, (int)b.y, (int)b.z, (int)b.w, 0, 0, 0, 0};
   // operand formats 4 = e2m1 for A and B, unit (E8M0 127) block scales
-  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(av, bv, c, 4, 4, 0, 127, 0, 127);
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, c, 4, 4, 0, 127, 0, 127);
 }
 
 __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
-  __shared__ __align__(16) uint8_t sA[2][TM * KB];
-  __shared__ __align__(16) uint8_t sB[2][TN * KB];
+  // one LDS array per ring slot and operand: every access below names its
+  // array, so the compiler can tell a slot being read from the slots the
+  // direct-to-LDS loads are still filling
+  __shared__ __align__(16) uint8_t sA0[TM * KB], sA1[TM * KB], sA2[TM * KB], sA3[TM * KB];
+  __shared__ __align__(16) uint8_t sB0[TN * KB], sB1[TN * KB], sB2[TN * KB], sB3[TN * KB];
   __shared__ uint64_t sP[TM][2];       // rho^{y^mu} bits of the tile's 128 columns
+  static_assert(kStages == 4, "one named array per slot");
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
@@ -68,72 +99,96 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     sP[r][w] = v;
   }
 
-  // loader: 128 rows x 4 chunks of 16 bytes per operand; 2 rows per thread
-  const int lrow = tid >> 2, lch = (tid & 3) * 16;
-  uint4 ra[2], rb[2];
-  auto gload = [&](int ks) {
+  // Loads: a wave moves rows 32*wave .. 32*wave+31 of each operand, 16 rows
+  // (1 KB) per instruction; lane l fills LDS bytes 16*l of the 1 KB, i.e. row
+  // l >> 2, physical chunk l & 3, which holds logical chunk (l & 3) ^ swz(row)
+  // of that row (the XOR swizzle keeps the MFMA operand reads conflict-free).
+  const uint8_t *srcA[2], *srcB[2];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int r = lrow + 64 * h;
-      const int gm = m0 + r, gn = n0 + r;
-      ra[h] = gm < p.M ? *reinterpret_cast<const uint4 *>(p.A + (size_t)gm * p.lda + ks * KB + lch)
-                       : make_uint4(0, 0, 0, 0);
-      rb[h] = gn < p.N ? *reinterpret_cast<const uint4 *>(p.B + (size_t)gn * p.ldb + ks * KB + lch)
-                       : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int r = lrow + 64 * h;
-      *reinterpret_cast<uint4 *>(&sA[buf][r * KB + lch]) = ra[h];
-      *reinterpret_cast<uint4 *>(&sB[buf][r * KB + lch]) = rb[h];
-    }
-  };
-
-  v4f acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
-
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  const int arow = lane & 15, achunk = (lane >> 4) * 16;
-  for (int ks = 0; ks < p.ksteps; ++ks) {
-    const int cur = ks & 1;
-    if (ks + 1 < p.ksteps) gload(ks + 1);
-    uint4 a[4], b[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      a[i] = *reinterpret_cast<const uint4 *>(&sA[cur][(wm * 64 + i * 16 + arow) * KB + achunk]);
-      b[i] = *reinterpret_cast<const uint4 *>(&sB[cur][(wn * 64 + i * 16 + arow) * KB + achunk]);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = mfma_fp4(a[i], b[j], acc[i][j]);
-    if (ks + 1 < p.ksteps) sstore(cur ^ 1);
-    __syncthreads();
+  for (int h = 0; h < 2; ++h) {
+    const int r = 32 * wave + 16 * h + (lane >> 2);
+    const int c = (lane & 3) ^ swz(r);
+    srcA[h] = p.A + (size_t)min(m0 + r, p.M - 1) * p.lda + c * 16;
+    srcB[h] = p.B + (size_t)min(n0 + r, p.N - 1) * p.ldb + c * 16;
   }
+  auto issue = [&](int ks, uint8_t *dA, uint8_t *dB) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      dma16(srcA[h] + ks * KB, dA + (2 * wave + h) * 1024);
+      dma16(srcB[h] + ks * KB, dB + (2 * wave + h) * 1024);
+    }
+  };
+
+  v16f acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = (v16f){};
+
+  const int arow = lane & 31, ahalf = lane >> 5;
+  auto compute = [&](const uint8_t *tA, const uint8_t *tB) {
+#pragma unroll
+    for (int kh = 0; kh < 2; ++kh) {
+      const int ch = 2 * kh + ahalf;   // 16-byte chunk of the 64-byte K step
+      uint4 a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int ra_ = wm * 64 + i * 32 + arow, rb_ = wn * 64 + i * 32 + arow;
+        a[i] = *reinterpret_cast<const uint4 *>(&tA[ra_ * KB + ((ch ^ swz(ra_)) * 16)]);
+        b[i] = *reinterpret_cast<const uint4 *>(&tB[rb_ * KB + ((ch ^ swz(rb_)) * 16)]);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = mfma_fp4(a[i], b[j], acc[i][j]);
+    }
+  };
+
+  const int nks = p.ksteps;
+  if (0 < nks) issue(0, sA0, sB0);
+  if (1 < nks) issue(1, sA1, sB1);
+  if (2 < nks) issue(2, sA2, sB2);
+  // Step ks: wait until this wave's loads of step ks are done (at most 4
+  // loads per later step still in flight), barrier (every wave's loads of
+  // step ks have landed and every wave has consumed step ks-1, whose slot is
+  // refilled next), then compute.  A plain s_barrier: the fence of
+  // __syncthreads would also wait for the loads of later steps.
+  auto step = [&](int ks, const uint8_t *tA, const uint8_t *tB, uint8_t *nA, uint8_t *nB) {
+    const int after = min(kStages - 2, nks - 1 - ks);
+    if (after >= 2)
+      wait_vm<8>();
+    else if (after == 1)
+      wait_vm<4>();
+    else
+      wait_vm<0>();
+    __builtin_amdgcn_s_barrier();
+    if (ks + kStages - 1 < nks) issue(ks + kStages - 1, nA, nB);
+    compute(tA, tB);
+  };
+  for (int ks = 0; ks < nks; ks += 4) {
+    step(ks, sA0, sB0, sA3, sB3);
+    if (ks + 1 < nks) step(ks + 1, sA1, sB1, sA0, sB0);
+    if (ks + 2 < nks) step(ks + 2, sA2, sB2, sA1, sB1);
+    if (ks + 3 < nks) step(ks + 3, sA3, sB3, sA2, sB2);
+  }
+  __syncthreads();
 
   // ---- epilogue ---------------------------------------------------------------
-  // lane holds z for column n0 + wn*64 + j*16 + (lane & 15) and rows
-  // m0 + wm*64 + i*16 + 4*(lane >> 4) + e, e = 0..3, in acc[i][j][e]
-  uint16_t *sbits = reinterpret_cast<uint16_t *>(&sA[0][0]);   // [128 rows][8 chunks of 16 columns]
-  const int lg = lane >> 4, lc = lane & 15;
+  // lane holds z for column n0 + wn*64 + j*32 + (lane & 31) and rows
+  // m0 + wm*64 + i*32 + 8*(e >> 2) + 4*(lane >> 5) + (e & 3) in acc[i][j][e]
+  uint32_t *sbits = reinterpret_cast<uint32_t *>(sA0);   // [128 rows][4 chunks of 32 columns]
+  const int lh = lane >> 5, lc = lane & 31;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int col = n0 + wn * 64 + j * 16 + lc;
+      for (int e = 0; e < 16; ++e) {
+        const int col = n0 + wn * 64 + j * 32 + lc;
         const uint64_t bal = __ballot(col < p.N && acc[i][j][e] >= 0.f);
         if (lc == 0) {
-          const int rl = wm * 64 + i * 16 + 4 * lg + e;
-          sbits[rl * 8 + wn * 4 + j] = (uint16_t)(bal >> (16 * lg));
+          const int rl = wm * 64 + i * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
+          sbits[rl * 4 + wn * 2 + j] = (uint32_t)(bal >> (32 * lh));
         }
       }
 
@@ -141,38 +196,58 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     const int gcol0 = n0 + wn * 64;   // the wave's 64 columns are one group
     if (gcol0 < p.N) {
       const int g = gcol0 >> 6;
+      // key of each of the lane's 32 rows q = 16*i + e over its 2 columns
+      uint32_t v[32];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int rl = wm * 64 + i * 16 + 4 * lg + e;
+        for (int e = 0; e < 16; ++e) {
+          const int rl = wm * 64 + i * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
           const uint64_t rho = sP[rl][wn];
           uint32_t key = 0xFFFFFFFFu;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int kl = j * 16 + lc;              // column within the group
+          for (int j = 0; j < 2; ++j) {
+            const int kl = j * 32 + lc;              // column within the group
             const int zz = (int)acc[i][j][e];
             const bool rpos = (rho >> kl) & 1ull;
             const bool wrong = rpos ? (zz < 0) : (zz > 0);
             const uint32_t kk = ((uint32_t)(zz < 0 ? -zz : zz) << 8) | (uint32_t)kl;
             key = wrong ? min(key, kk) : key;
           }
-#pragma unroll
-          for (int off = 1; off < 16; off <<= 1) key = min(key, (uint32_t)__shfl_xor((int)key, off, 64));
-          const int m = m0 + rl;
-          if (lc == 0 && m < p.M)
-            p.kstar[(size_t)g * p.ldk + m] = key == 0xFFFFFFFFu ? (int16_t)-1 : (int16_t)(key & 0xFFu);
+          v[i * 16 + e] = key;
         }
+      // butterfly reduce-scatter over the 32 lanes of a half-wave: at distance
+      // d a lane keeps half of its rows (the upper half if bit d of its lane
+      // is set) and takes the minimum with the partner's copy of those rows;
+      // afterwards lane lc holds the minimum over all 64 columns of row q = lc
+#pragma unroll
+      for (int d = 16; d >= 1; d >>= 1) {
+        const uint32_t upm = (lc & d) ? 0xFFFFFFFFu : 0u;
+#pragma unroll
+        for (int k = 0; k < d; ++k) {
+          // swap v[k], v[k+d] on upper lanes with a mask (no selects between
+          // array elements, which the compiler would turn into indexing)
+          const uint32_t x = (v[k] ^ v[k + d]) & upm;
+          const uint32_t send = v[k + d] ^ x;
+          const uint32_t keep = v[k] ^ x;
+          const uint32_t recv = (uint32_t)__shfl_xor((int)send, d, 64);
+          v[k] = min(keep, recv);
+        }
+      }
+      const int i = lc >> 4, e = lc & 15;
+      const int rl = wm * 64 + i * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
+      const int m = m0 + rl;
+      if (m < p.M) p.kstar[(size_t)g * p.ldk + m] = v[0] == 0xFFFFFFFFu ? (int16_t)-1 : (int16_t)(v[0] & 0xFFu);
     }
   } else if (p.mode == kFwdWriteZ) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int m = m0 + wm * 64 + i * 16 + 4 * lg + e;
-          const int col = n0 + wn * 64 + j * 16 + lc;
+        for (int e = 0; e < 16; ++e) {
+          const int m = m0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
+          const int col = n0 + wn * 64 + j * 32 + lc;
           if (m < p.M && col < p.N) p.z[(size_t)m * p.ldz + col] = (int16_t)(int)acc[i][j][e];
         }
   }
@@ -183,7 +258,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     const int r = tid >> 1, w = tid & 1;
     const int m = m0 + r, wg = (n0 >> 6) + w;
     if (m < p.M && wg < p.words_out) {
-      const uint64_t v = *reinterpret_cast<const uint64_t *>(&sbits[r * 8 + w * 4]);
+      const uint64_t v = *reinterpret_cast<const uint64_t *>(&sbits[r * 4 + w * 2]);
       p.abits[(size_t)m * p.words_out + wg] = v;
     }
   }
@@ -192,7 +267,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     const int r = tid >> 1, h = tid & 1;
     const int m = m0 + r;
     if (m < p.M) {
-      const uint64_t bits = *reinterpret_cast<const uint64_t *>(&sbits[r * 8 + h * 4]);
+      const uint64_t bits = *reinterpret_cast<const uint64_t *>(&sbits[r * 4 + h * 2]);
       const int cbase = n0 + h * 64;
       const int nv = min(max(p.N - cbase, 0), 64);
       const uint64_t valid = nv == 64 ? ~0ull : ((1ull << nv) - 1ull);

@@ -63,9 +63,12 @@ __device__ __forceinline__ int wave_sum(int v) {
 
 // Grid: ceil(n / 4) blocks of 256 threads, one wave per pattern.
 __global__ __launch_bounds__(256) void loss_select_kernel(LossSelectArgs p) {
+  __shared__ int cnt[3];
+  if (threadIdx.x < 3) cnt[threadIdx.x] = 0;
+  __syncthreads();
   const int mu = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  if (mu >= p.n) return;
+  if (mu < p.n) {
   const bool select_only = p.yhat == nullptr;   // upd already computed
   const int label = p.y[mu];
   const int yl = min(max(label, 0), p.c - 1);      // stay inside P on a bad label
@@ -107,20 +110,33 @@ __global__ __launch_bounds__(256) void loss_select_kernel(LossSelectArgs p) {
     if (!select_only) {
       p.err[mu] = err ? 1 : 0;
       p.upd[mu] = upd ? 1 : 0;
-      if (err) atomicAdd(p.stats + 0, 1);
-      if (upd) atomicAdd(p.stats + 1, 1);
+      if (err) atomicAdd(&cnt[0], 1);
+      if (upd) atomicAdd(&cnt[1], 1);
     }
-    if (nsel) atomicAdd(p.stats + 2, nsel);
+    if (nsel) atomicAdd(&cnt[2], nsel);
+  }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {   // one global atomic per counter and work-group
+    if (cnt[0]) atomicAdd(p.stats + 0, cnt[0]);
+    if (cnt[1]) atomicAdd(p.stats + 1, cnt[1]);
+    if (cnt[2]) atomicAdd(p.stats + 2, cnt[2]);
   }
 }
 
 __global__ __launch_bounds__(256) void eval_count_kernel(const int32_t *yhat, int c, const int32_t *y,
                                                          int n, int32_t *correct) {
+  __shared__ int cnt;
+  if (threadIdx.x == 0) cnt = 0;
+  __syncthreads();
   const int mu = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  if (mu >= n) return;
-  const Top2 t = wave_top2(yhat + (size_t)mu * c, c, lane);
-  if (lane == 0 && t.i1 == y[mu]) atomicAdd(correct, 1);
+  if (mu < n) {
+    const Top2 t = wave_top2(yhat + (size_t)mu * c, c, lane);
+    if (lane == 0 && t.i1 == y[mu]) atomicAdd(&cnt, 1);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0 && cnt) atomicAdd(correct, cnt);
 }
 
 }  // namespace

@@ -326,7 +326,13 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   }
 
   nreinf = wave_sum(nreinf);
-  if (lane == 0 && nreinf) atomicAdd(U.stats + 3, nreinf);
+  if (lane == 0) part[wave] = nreinf;
+  __syncthreads();
+  if (tid == 0) {
+    int t = 0;
+    for (int w = 0; w < kWaves; ++w) t += part[w];
+    if (t) atomicAdd(U.stats + 3, t);   // one atomic per work-group
+  }
 }
 
 }  // namespace
