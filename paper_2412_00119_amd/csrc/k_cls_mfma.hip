@@ -4,13 +4,13 @@
 //
 // A work-group owns 16 patterns and all classes, taken CB blocks of 16
 // classes per pass (CB is a template parameter sized to the class count).
-// The four waves split K (wave w takes K steps w, w+4, ...), each keeping
-// one 16x16 accumulator per block of 16 classes, and prefetch the next K
-// step's operands while the current one runs on the matrix cores; loads are
-// unconditional (indices clamped, data masked) so the prefetch is not
-// serialised by conservative waits.  The
-// partial sums are exact integers, so adding them in LDS with float atomics
-// gives the same y_hat in any order.  After a barrier each wave takes four of the
+// Its sixteen waves split K (wave w takes K steps w, w+16, ...); for each
+// step a wave loads its operands, waits and runs one MFMA per class block,
+// and the other fifteen waves on the CU hide that latency.  Loads are
+// unconditional (indices clamped, data masked).  The partial sums are exact
+// integers, so they are converted to int32 and added with integer LDS
+// atomics (float LDS atomics are far slower), giving the same y_hat in any
+// order.  After a barrier each wave takes one of the
 // patterns: first argmax (lowest class on ties), the two largest values
 // (tau = top1 - top2, 0 on a tie), err = (pred != y), upd = err or
 // tau < ceil(r K_l).  Patterns outside M_l get no selected perceptron
@@ -56,9 +56,11 @@ __device__ __forceinline__ int wave_sum(int v) {
   return v;
 }
 
+constexpr int kWaves = 16;
+
 template <int CB>
-__global__ __launch_bounds__(256) void cls_fp4_kernel(ClsArgs p) {
-  __shared__ float red[16][CB * 16];
+__global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsArgs p) {
+  __shared__ int red[16][CB * 16];
   __shared__ int cnt[4];   // block totals of err, upd, selected, correct
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int m0 = blockIdx.x * 16;
@@ -71,7 +73,7 @@ __global__ __launch_bounds__(256) void cls_fp4_kernel(ClsArgs p) {
 
   for (int cb0 = 0; cb0 < nblk; cb0 += CB) {
     const int nb = min(CB, nblk - cb0);
-    for (int i = tid; i < 16 * CB * 16; i += 256) (&red[0][0])[i] = 0.f;
+    for (int i = tid; i < 16 * CB * 16; i += 64 * kWaves) (&red[0][0])[i] = 0;
     v4f acc[CB];
 #pragma unroll
     for (int j = 0; j < CB; ++j) acc[j] = (v4f){0.f, 0.f, 0.f, 0.f};
@@ -83,25 +85,14 @@ __global__ __launch_bounds__(256) void cls_fp4_kernel(ClsArgs p) {
       bmask[j] = cls < p.c ? 0xFFFFFFFFu : 0u;
       brow[j] = p.P + (size_t)min(cls, p.c - 1) * p.ldp + lk;
     }
-    uint4 a_cur, b_cur[CB], a_nxt, b_nxt[CB];
-    auto load = [&](uint4 &a, uint4 (&b)[CB], int ks) {
-      a = *reinterpret_cast<const uint4 *>(arow + ks * 64);
+    for (int ks = wave; ks < p.ksteps; ks += kWaves) {
+      const uint4 a = masked(*reinterpret_cast<const uint4 *>(arow + ks * 64), amask);
+      uint4 b[CB];
 #pragma unroll
       for (int j = 0; j < CB; ++j) b[j] = *reinterpret_cast<const uint4 *>(brow[j] + ks * 64);
-    };
-    int ks = wave;
-    if (ks < p.ksteps) load(a_cur, b_cur, ks);
-    while (ks < p.ksteps) {
-      const int kn = ks + 4;
-      if (kn < p.ksteps) load(a_nxt, b_nxt, kn);
-      const uint4 am4 = masked(a_cur, amask);
 #pragma unroll
       for (int j = 0; j < CB; ++j)
-        if (j < nb) acc[j] = mfma_fp4(am4, masked(b_cur[j], bmask[j]), acc[j]);
-      a_cur = a_nxt;
-#pragma unroll
-      for (int j = 0; j < CB; ++j) b_cur[j] = b_nxt[j];
-      ks = kn;
+        if (j < nb) acc[j] = mfma_fp4(a, masked(b[j], bmask[j]), acc[j]);
     }
     __syncthreads();   // red is zeroed
     // lane holds classes (cb0 + j)*16 + (lane & 15) of patterns 4*(lane >> 4) + e
@@ -109,12 +100,12 @@ __global__ __launch_bounds__(256) void cls_fp4_kernel(ClsArgs p) {
     for (int j = 0; j < CB; ++j)
       if (j < nb)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) atomicAdd(&red[4 * (lane >> 4) + e][j * 16 + lr], acc[j][e]);
+        for (int e = 0; e < 4; ++e) atomicAdd(&red[4 * (lane >> 4) + e][j * 16 + lr], (int)acc[j][e]);
     __syncthreads();
-    for (int i = tid; i < 16 * CB * 16; i += 256) {
+    for (int i = tid; i < 16 * CB * 16; i += 64 * kWaves) {
       const int r = i / (CB * 16), cl = i % (CB * 16);
       const int m = m0 + r, cls = cb0 * 16 + cl;
-      if (m < p.n && cls < p.c) p.yhat[(size_t)m * p.ldo + cls] = (int32_t)red[r][cl];
+      if (m < p.n && cls < p.c) p.yhat[(size_t)m * p.ldo + cls] = red[r][cl];
     }
     __syncthreads();
   }
@@ -122,7 +113,7 @@ __global__ __launch_bounds__(256) void cls_fp4_kernel(ClsArgs p) {
   if (tid < 4) cnt[tid] = 0;
   __syncthreads();   // y_hat of the 16 patterns is complete (global writes, same work-group)
 
-  for (int r = wave; r < 16; r += 4) {
+  for (int r = wave; r < 16; r += kWaves) {
     const int mu = m0 + r;
     if (mu >= p.n) break;
     Top2 t{INT_MIN, INT_MAX, INT_MIN};
@@ -190,17 +181,15 @@ __global__ __launch_bounds__(256) void cls_fp4_kernel(ClsArgs p) {
 hipError_t launch_cls_fp4(const ClsArgs &a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
   const int nblk = (a.c + 15) / 16;
-  const dim3 grid((a.n + 15) / 16), block(256);
+  const dim3 grid((a.n + 15) / 16), block(64 * kWaves);
   if (nblk <= 1)
     hipLaunchKernelGGL(cls_fp4_kernel<1>, grid, block, 0, s, a);
   else if (nblk <= 2)
     hipLaunchKernelGGL(cls_fp4_kernel<2>, grid, block, 0, s, a);
   else if (nblk <= 4)
     hipLaunchKernelGGL(cls_fp4_kernel<4>, grid, block, 0, s, a);
-  else if (nblk <= 8)
-    hipLaunchKernelGGL(cls_fp4_kernel<8>, grid, block, 0, s, a);
   else
-    hipLaunchKernelGGL(cls_fp4_kernel<16>, grid, block, 0, s, a);
+    hipLaunchKernelGGL(cls_fp4_kernel<8>, grid, block, 0, s, a);
   return hipGetLastError();
 }
 
