@@ -125,8 +125,9 @@ typedef struct bmlp_config {
  *                    upd_l  uint8  [max_batch]   1 = pattern in M_l
  *                    kstar_l int16 [groups][max_batch]  easiest wrong
  *                           perceptron of each group as an offset in the
- *                           group; -1 when the group has none or the pattern
- *                           is not in M_l (the pairs of U_l, Algorithm 2)
+ *                           group (-1 when the group has none), for every
+ *                           pattern; U_l (Algorithm 2) is its restriction to
+ *                           the patterns with upd_l = 1
  *                    a_l as fp4 (off_aq, uint8 [max_batch][ldq_out]).
  */
 typedef struct bmlp_layer_info {

@@ -152,8 +152,8 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
   p->ldz = 64 * words64(kmax);
   p->off_z = wo;
   wo = align256(wo + (size_t)nb * p->ldz * 2);
-  p->off_yhat = wo;
-  wo = align256(wo + (size_t)nb * p->c * 4);
+  p->off_yhat = wo;   // [L][max_batch][c]
+  wo = align256(wo + (size_t)p->L * nb * p->c * 4);
   p->ws_bytes = wo;
   return BMLP_OK;
 }
@@ -194,15 +194,23 @@ int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32
       f.afp4 = ctx->ws + lp.off_aq; f.ld_af = lp.ldq_out;
       f.mode = kFwdPlain;
       BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s, launch_fwd_fp4(f, s));
-      ClsArgs c{};
-      c.A = f.afp4; c.lda = lp.ldq_out;
-      c.P = ctx->state + lp.off_pq; c.ldp = lp.ldq_out;
-      c.n = n; c.c = p.c; c.ksteps = lp.ldq_out / 64;
-      c.yhat = yhat_out ? yhat_out + (size_t)(l - 1) * n * p.c : yh_ws; c.ldo = p.c;
-      c.mode = correct ? kClsEval : kClsYhatOnly;
-      c.y = y; c.correct = correct ? correct + (l - 1) : nullptr;
-      BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_cls_fp4(c, s));
       aq_prev = f.afp4;
+    }
+    // every layer's local classifier in one launch per kMaxClsLayers layers
+    ClsBatch cb{};
+    cb.n = n; cb.c = p.c; cb.y = y; cb.mode = correct ? kClsEval : kClsYhatOnly;
+    for (int l = 1; l <= p.L; ++l) {
+      const LayerPlan &lp = p.layer[l - 1];
+      ClsLayer &c = cb.L[cb.nl++];
+      c.A = ctx->ws + lp.off_aq; c.lda = lp.ldq_out;
+      c.P = ctx->state + lp.off_pq; c.ldp = lp.ldq_out;
+      c.ksteps = lp.ldq_out / 64;
+      c.yhat = yhat_out ? yhat_out + (size_t)(l - 1) * n * p.c : yh_ws + (size_t)(l - 1) * p.max_batch * p.c;
+      c.correct = correct ? correct + (l - 1) : nullptr;
+      if (cb.nl == kMaxClsLayers || l == p.L) {
+        BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_cls_fp4(cb, s));
+        cb.nl = 0;
+      }
     }
     return BMLP_OK;
   }
@@ -393,7 +401,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
     ls.err = err; ls.upd = upd; ls.kstar = kstar; ls.ldk = p.max_batch; ls.stats = stats;
     if (mfma) {
       const bool fused = lp.gamma == 64;
-      // Algorithm 1 lines 8-9 (+ Algorithm 2 when fused)
+      // Algorithm 1 lines 8-9, and Algorithm 2's choice when fused
       FwdArgs f{};
       f.A = aq_prev; f.lda = lp.ldq_in;
       f.B = ctx->state + lp.off_wq; f.ldb = lp.ldq_in;
@@ -405,19 +413,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
       f.y = d_y; f.Pbits = P; f.c = p.c;
       f.z = z; f.ldz = p.ldz;
       BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s, launch_fwd_fp4(f, s));
-      // Algorithm 1 lines 10-15
-      ClsArgs c{};
-      c.A = f.afp4; c.lda = lp.ldq_out;
-      c.P = ctx->state + lp.off_pq; c.ldp = lp.ldq_out;
-      c.n = n; c.c = p.c; c.ksteps = lp.ldq_out / 64;
-      c.yhat = yh; c.ldo = p.c;
-      c.mode = kClsTrain;
-      c.y = d_y; c.thr = lp.robust_thr;
-      c.err = err; c.upd = upd;
-      c.kstar = fused ? kstar : nullptr; c.ldk = p.max_batch; c.groups = lp.groups;
-      c.stats = stats;
-      BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_cls_fp4(c, s));
-      if (!fused) {   // Algorithm 2 from the stored z
+      if (!fused) {   // Algorithm 2 from the stored z, before the next layer reuses it
         ls.yhat = nullptr;
         BMLP_TIMED(ctx, BMLP_KERNEL_SELECT, s, launch_loss_select(ls, s));
       }
@@ -433,6 +429,25 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
     }
     a_prev = a;
   }
+  if (mfma) {
+    // Algorithm 1 lines 10-15 for every layer, one launch per kMaxClsLayers layers
+    ClsBatch cb{};
+    cb.n = n; cb.c = p.c; cb.y = d_y; cb.mode = kClsTrain;
+    for (int l = 1; l <= p.L; ++l) {
+      const LayerPlan &lp = p.layer[l - 1];
+      ClsLayer &c = cb.L[cb.nl++];
+      c.A = ctx->ws + lp.off_aq; c.lda = lp.ldq_out;
+      c.P = ctx->state + lp.off_pq; c.ldp = lp.ldq_out;
+      c.ksteps = lp.ldq_out / 64; c.thr = lp.robust_thr;
+      c.yhat = yh + (size_t)(l - 1) * p.max_batch * p.c;
+      c.err = ctx->ws + lp.off_err; c.upd = ctx->ws + lp.off_upd;
+      c.stats = d_stats + 4 * (l - 1);
+      if (cb.nl == kMaxClsLayers || l == p.L) {
+        BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_cls_fp4(cb, s));
+        cb.nl = 0;
+      }
+    }
+  }
   // Algorithm 3 for every layer (each layer's forward above used its
   // pre-step weights; the updates touch only H_l and W_l).
   UpdateBatch ub{};
@@ -447,6 +462,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
     u.a32 = reinterpret_cast<const uint32_t *>(l == 1 ? d_x : reinterpret_cast<const uint64_t *>(
                                                                ctx->ws + p.layer[l - 2].off_a));
     u.kstar = reinterpret_cast<const int16_t *>(ctx->ws + lp.off_kstar);
+    u.upd = ctx->ws + lp.off_upd;
     u.P = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p);
     u.stats = d_stats + 4 * (l - 1);
     u.ld_h = lp.ld_h; u.nw32 = 2 * lp.words_in; u.words_out = lp.words_out;

@@ -89,24 +89,30 @@ hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s);
 hipError_t launch_fp4_rows(const uint64_t *bits, int words, int K, int R, uint8_t *q, int ldq,
                            int32_t *zero, int nzero, hipStream_t s);
 
-// Classifier on the matrix cores, then the local error signal.
+// Classifier on the matrix cores, then the local error signal, for up to
+// kMaxClsLayers layers in one launch (ceil(n / 16) work-groups per layer).
 enum { kClsTrain = 0, kClsYhatOnly = 1, kClsEval = 2 };
-struct ClsArgs {
+struct ClsLayer {
   const uint8_t *A; int lda;        // a_l fp4 [n][lda]
   const uint8_t *P; int ldp;        // P_l fp4 [c][ldp]
-  int n, c, ksteps;
-  int32_t *yhat; int ldo;           // y_hat int32 [n][ldo]
-  int mode;
-  const int32_t *y; int thr;
-  uint8_t *err, *upd;
-  int16_t *kstar; int ldk, groups;  // train: masks patterns outside M (may be null)
-  int32_t *stats;                   // train: this layer's [4]
-  int32_t *correct;                 // eval
+  int ksteps, thr;
+  int32_t *yhat;                    // y_hat int32 [n][c]: output (kClsYhatOnly), or
+                                    // scratch when c needs several passes
+  uint8_t *err, *upd;               // train
+  int32_t *stats;                   // train: this layer's [4], adds [0] and [1]
+  int32_t *correct;                 // eval: adds the correct count
 };
-hipError_t launch_cls_fp4(const ClsArgs &a, hipStream_t s);
+constexpr int kMaxClsLayers = 8;
+struct ClsBatch {
+  ClsLayer L[kMaxClsLayers];
+  int nl, n, c, mode;
+  const int32_t *y;
+};
+hipError_t launch_cls_fp4(const ClsBatch &a, hipStream_t s);
 
-// 01-loss, margin, M and the easiest wrong perceptron per group.  With
-// yhat == nullptr the kernel only selects, for the patterns whose upd is set.
+// 01-loss, margin and M (when yhat is given), and the easiest wrong
+// perceptron of every group for every pattern (U_l is its restriction to the
+// patterns in M, which the update kernel applies).
 struct LossSelectArgs {
   const int32_t *yhat; int c;
   const int16_t *z; int ldz;
@@ -130,9 +136,10 @@ struct UpdLayer {
   uint32_t *W32;
   uint8_t *Wq; int ldq;    // W_l as fp4 [K_l][ldq]
   const uint32_t *a32;     // a_{l-1} bit rows as 32-bit words [n][nw32]
-  const int16_t *kstar;    // [groups][ldk]
+  const int16_t *kstar;    // [groups][ldk], for every pattern
+  const uint8_t *upd;      // [n]: only patterns in M_l are used
   const uint64_t *P;
-  int32_t *stats;          // this layer's [4]; reads [1] (|M|), adds [3]
+  int32_t *stats;          // this layer's [4]; reads [1] (|M|), adds [2] and [3]
   int ld_h, nw32, words_out, k_in, groups, gamma;
   int chunks, block0;      // filled by launch_update
   uint32_t t_hi, t_lo;     // T_l >> 24 (0..256) and T_l & 0xFFFFFF

@@ -1,12 +1,13 @@
 // Local error signal and perceptron selection (Algorithm 1 01-loss and
 // robustness test, Eq. 1; Algorithm 2 easiest-perceptron choice).
 //
-// One wave per pattern.  The wave finds the first argmax of y_hat and the two
-// largest values (tau = top1 - top2, 0 on a tie), sets err = (pred != y) and
-// upd = err or tau < ceil(r K_l).  For a pattern in M it then takes, in every
-// group of gamma contiguous perceptrons, the one with the largest negative
-// stability delta_k = z_k rho^{y}_k, i.e. the smallest |z_k| among those whose
-// sign disagrees with rho^{y}_k, lowest k on ties; delta = 0 is not eligible.
+// One wave per pattern.  Given y_hat, the wave finds the first argmax and the
+// two largest values (tau = top1 - top2, 0 on a tie), sets err = (pred != y)
+// and upd = err or tau < ceil(r K_l).  For every pattern it then takes, in
+// every group of gamma contiguous perceptrons, the one with the largest
+// negative stability delta_k = z_k rho^{y}_k, i.e. the smallest |z_k| among
+// those whose sign disagrees with rho^{y}_k, lowest k on ties; delta = 0 is
+// not eligible.  The update keeps only the patterns in M.
 #include <limits.h>
 
 #include "bmlp_internal.h"
@@ -63,26 +64,23 @@ __device__ __forceinline__ int wave_sum(int v) {
 
 // Grid: ceil(n / 4) blocks of 256 threads, one wave per pattern.
 __global__ __launch_bounds__(256) void loss_select_kernel(LossSelectArgs p) {
-  __shared__ int cnt[3];
-  if (threadIdx.x < 3) cnt[threadIdx.x] = 0;
+  __shared__ int cnt[2];
+  if (threadIdx.x < 2) cnt[threadIdx.x] = 0;
   __syncthreads();
   const int mu = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (mu < p.n) {
-  const bool select_only = p.yhat == nullptr;   // upd already computed
+  const bool select_only = p.yhat == nullptr;
   const int label = p.y[mu];
   const int yl = min(max(label, 0), p.c - 1);      // stay inside P on a bad label
-  bool err = false, upd;
-  if (select_only) {
-    upd = p.upd[mu] != 0;
-  } else {
+  bool err = false, upd = false;
+  if (!select_only) {
     const Top2 t = wave_top2(p.yhat + (size_t)mu * p.c, p.c, lane);
     err = t.i1 != label;
     upd = err || (t.v1 - t.v2) < p.thr;
   }
-  int nsel = 0;
   int16_t *ks = p.kstar + mu;   // column mu of kstar [groups][ldk]
-  if (upd) {
+  {
     const int16_t *zr = p.z + (size_t)mu * p.ldz;
     const uint64_t *rho = p.P + (size_t)yl * p.words_out;
     for (int g = lane; g < p.groups; g += 64) {
@@ -100,27 +98,19 @@ __global__ __launch_bounds__(256) void loss_select_kernel(LossSelectArgs p) {
         }
       }
       ks[(size_t)g * p.ldk] = (int16_t)best;
-      nsel += best >= 0;
     }
-  } else {
-    for (int g = lane; g < p.groups; g += 64) ks[(size_t)g * p.ldk] = (int16_t)-1;
   }
-  nsel = wave_sum(nsel);
-  if (lane == 0) {
-    if (!select_only) {
-      p.err[mu] = err ? 1 : 0;
-      p.upd[mu] = upd ? 1 : 0;
-      if (err) atomicAdd(&cnt[0], 1);
-      if (upd) atomicAdd(&cnt[1], 1);
-    }
-    if (nsel) atomicAdd(&cnt[2], nsel);
+  if (lane == 0 && !select_only) {
+    p.err[mu] = err ? 1 : 0;
+    p.upd[mu] = upd ? 1 : 0;
+    if (err) atomicAdd(&cnt[0], 1);
+    if (upd) atomicAdd(&cnt[1], 1);
   }
   }
   __syncthreads();
   if (threadIdx.x == 0) {   // one global atomic per counter and work-group
     if (cnt[0]) atomicAdd(p.stats + 0, cnt[0]);
     if (cnt[1]) atomicAdd(p.stats + 1, cnt[1]);
-    if (cnt[2]) atomicAdd(p.stats + 2, cnt[2]);
   }
 }
 

@@ -10,7 +10,8 @@
 // whose M_l is empty is left untouched.
 //
 // Work item: (layer, group g, 2048-column chunk); a work-group of 8 waves.
-// The group's selections are bucketed by perceptron in LDS (counting sort),
+// The group's selections U_l (each pattern in M_l with a wrong perceptron in
+// the group) are bucketed by perceptron in LDS (counting sort),
 // then each wave walks whole rows with a lane owning 32 consecutive columns
 // (one 32-bit word of a_{l-1}).  With x = a-word XOR [rho = -1] the number
 // of +1 contributions per column is counted in bit-sliced form (plane p holds
@@ -107,13 +108,25 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   const int16_t *kcol = U.kstar + (size_t)g * p.ldk;
 
   // ---- bucket the selections of group g by perceptron (counting sort) -------
+  __shared__ int s_sel;
+  if (tid == 0) s_sel = 0;
   for (int r = tid; r < gamma; r += kThreads) bucket[r] = 0;
   __syncthreads();
+  // U_l: the selections of the patterns in M_l
+  int nsel = 0;
   for (int mu = tid; mu < p.n; mu += kThreads) {
-    const int ks = kcol[mu];
-    if (ks >= 0) atomicAdd(&bucket[ks], 1);
+    const int ks = U.upd[mu] ? kcol[mu] : -1;
+    if (ks >= 0) {
+      atomicAdd(&bucket[ks], 1);
+      ++nsel;
+    }
+  }
+  if (chunk == 0) {   // |U_l|, counted once per group
+    nsel = wave_sum(nsel);
+    if ((tid & 63) == 0 && nsel) atomicAdd(&s_sel, nsel);
   }
   __syncthreads();
+  if (chunk == 0 && tid == 0 && s_sel) atomicAdd(U.stats + 2, s_sel);
   {
     const int ch = (gamma + kThreads - 1) / kThreads;
     const int b0 = min(gamma, tid * ch), b1 = min(gamma, b0 + ch);
@@ -136,7 +149,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   }
   __syncthreads();
   for (int mu = tid; mu < p.n; mu += kThreads) {
-    const int ks = kcol[mu];
+    const int ks = U.upd[mu] ? kcol[mu] : -1;
     if (ks >= 0) {
       const int k = g * gamma + ks;
       const int yl = min(max(p.y[mu], 0), p.c - 1);   // stay inside P on a bad label

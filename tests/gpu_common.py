@@ -97,7 +97,15 @@ class Pair:
                                           err_msg=f"{tag} err_{l}")
             np.testing.assert_array_equal(g["upd"].cpu().numpy(), lt.upd.astype(np.uint8),
                                           err_msg=f"{tag} upd_{l}")
-            np.testing.assert_array_equal(g["kstar"].cpu().numpy(), lt.kstar, err_msg=f"{tag} kstar_{l}")
+            # the library keeps the selection of every pattern; U_l is its
+            # restriction to the patterns in M_l (checked through H and stats)
+            cfg = self.ora.cfg
+            raw = ob.select_easiest(lt.z, self.ora.P[l - 1], np.asarray(y), np.ones(len(y), bool),
+                                    cfg.gamma(self.widths[l]))
+            ks = g["kstar"].cpu().numpy()
+            np.testing.assert_array_equal(ks, raw, err_msg=f"{tag} kstar_{l}")
+            np.testing.assert_array_equal(np.where(lt.upd[:, None], ks, -1), lt.kstar,
+                                          err_msg=f"{tag} U_{l}")
             np.testing.assert_array_equal(st[l - 1], lt.stats, err_msg=f"{tag} stats_{l}")
         if check_state:
             self.check_state(tag)
