@@ -8,8 +8,8 @@
 // work-group computes a 128 x 128 tile of z (patterns x perceptrons) with
 // four waves of 64 x 64; K is walked in steps of 128 elements through a
 // ring of kStages LDS buffers filled by direct-to-LDS loads
-// (global_load_lds_dwordx4), kStages - 1 steps ahead of the matrix cores, with
-// one barrier per step.  Rows past the matrix end are clamped into range:
+// (global_load_lds_dwordx4) three steps ahead of the matrix cores, with one
+// barrier per step; operands are read from LDS one step ahead.  Rows past the matrix end are clamped into range:
 // they only feed outputs that are never stored.  The epilogue never writes z
 // to memory:
 //   * a_l as bit rows (wave ballots) and as fp4 rows for the next layer and
@@ -125,51 +125,101 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = (v16f){};
 
+  // operands of one K step: [kh][i] for the two 64-element halves
+  struct Ops {
+    uint4 a[2][2], b[2][2];
+  };
   const int arow = lane & 31, ahalf = lane >> 5;
-  auto compute = [&](const uint8_t *tA, const uint8_t *tB) {
+  auto read = [&](Ops &o, const uint8_t *tA, const uint8_t *tB) {
 #pragma unroll
     for (int kh = 0; kh < 2; ++kh) {
       const int ch = 2 * kh + ahalf;   // 16-byte chunk of the 64-byte K step
-      uint4 a[2], b[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         const int ra_ = wm * 64 + i * 32 + arow, rb_ = wn * 64 + i * 32 + arow;
-        a[i] = *reinterpret_cast<const uint4 *>(&tA[ra_ * KB + ((ch ^ swz(ra_)) * 16)]);
-        b[i] = *reinterpret_cast<const uint4 *>(&tB[rb_ * KB + ((ch ^ swz(rb_)) * 16)]);
+        o.a[kh][i] = *reinterpret_cast<const uint4 *>(&tA[ra_ * KB + ((ch ^ swz(ra_)) * 16)]);
+        o.b[kh][i] = *reinterpret_cast<const uint4 *>(&tB[rb_ * KB + ((ch ^ swz(rb_)) * 16)]);
       }
+    }
+  };
+  auto compute = [&](const Ops &o) {
+#pragma unroll
+    for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mfma_fp4(a[i], b[j], acc[i][j]);
-    }
+        for (int j = 0; j < 2; ++j) acc[i][j] = mfma_fp4(o.a[kh][i], o.b[kh][j], acc[i][j]);
   };
 
+  // Pipeline of step ks: the loads of step ks+3 are issued into the slot of
+  // step ks-1, the MFMAs of step ks run on operands read during step ks-1,
+  // and then the operands of step ks+1 are read from LDS (after the MFMAs in
+  // program order, so the reads complete under them and the next barrier).
+  // The slot of step ks-1 is free: its operands fed MFMAs issued before this
+  // step's barrier.
   const int nks = p.ksteps;
   if (0 < nks) issue(0, sA0, sB0);
   if (1 < nks) issue(1, sA1, sB1);
   if (2 < nks) issue(2, sA2, sB2);
-  // Step ks: wait until this wave's loads of step ks are done (at most 4
-  // loads per later step still in flight), barrier (every wave's loads of
-  // step ks have landed and every wave has consumed step ks-1, whose slot is
-  // refilled next), then compute.  A plain s_barrier: the fence of
-  // __syncthreads would also wait for the loads of later steps.
-  auto step = [&](int ks, const uint8_t *tA, const uint8_t *tB, uint8_t *nA, uint8_t *nB) {
-    const int after = min(kStages - 2, nks - 1 - ks);
+  // this wave's loads of step t are done when at most 4 * (steps issued
+  // after t) loads are in flight
+  auto wait_step = [&](int t, int issued_last) {
+    const int after = min(2, issued_last - t);
     if (after >= 2)
       wait_vm<8>();
     else if (after == 1)
       wait_vm<4>();
     else
       wait_vm<0>();
-    __builtin_amdgcn_s_barrier();
-    if (ks + kStages - 1 < nks) issue(ks + kStages - 1, nA, nB);
-    compute(tA, tB);
   };
-  for (int ks = 0; ks < nks; ks += 4) {
-    step(ks, sA0, sB0, sA3, sB3);
-    if (ks + 1 < nks) step(ks + 1, sA1, sB1, sA0, sB0);
-    if (ks + 2 < nks) step(ks + 2, sA2, sB2, sA1, sB1);
-    if (ks + 3 < nks) step(ks + 3, sA3, sB3, sA2, sB2);
+  Ops r0, r1;
+  if (0 < nks) {
+    wait_step(0, min(2, nks - 1));
+    __builtin_amdgcn_s_barrier();   // every wave's loads of step 0 have landed
+    read(r0, sA0, sB0);
+  }
+  // one step with every bound checked (used for the last few steps)
+  auto step = [&](int ks, Ops &cur, Ops &nxt, const uint8_t *rA, const uint8_t *rB, uint8_t *dA,
+                  uint8_t *dB) {
+    if (ks + 1 < nks) {
+      wait_step(ks + 1, min(ks + 2, nks - 1));
+      // A plain s_barrier: the fence of __syncthreads would also wait for
+      // the loads still in flight for later steps.
+      __builtin_amdgcn_s_barrier();
+      if (ks + 3 < nks) issue(ks + 3, dA, dB);
+    }
+    compute(cur);
+    __builtin_amdgcn_sched_barrier(0);   // keep the reads below the MFMAs
+    if (ks + 1 < nks) read(nxt, rA, rB);
+  };
+  // the same step in the steady state (steps ks+1..ks+3 exist): no branches,
+  // so the compiler can count the LDS reads in flight
+  // The sched_barrier(0) fences pin the order of the phases; otherwise the
+  // scheduler sinks the read-ahead to its use and the LDS latency reappears.
+  auto step_full = [&](int ks, Ops &cur, Ops &nxt, const uint8_t *rA, const uint8_t *rB, uint8_t *dA,
+                       uint8_t *dB) {
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vm<4>();   // step ks+1 landed; step ks+2 may still be in flight
+    __builtin_amdgcn_s_barrier();
+    issue(ks + 3, dA, dB);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(cur);
+    __builtin_amdgcn_sched_barrier(0);
+    read(nxt, rA, rB);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  int ks = 0;
+  for (; ks + 7 <= nks; ks += 4) {
+    step_full(ks, r0, r1, sA1, sB1, sA3, sB3);
+    step_full(ks + 1, r1, r0, sA2, sB2, sA0, sB0);
+    step_full(ks + 2, r0, r1, sA3, sB3, sA1, sB1);
+    step_full(ks + 3, r1, r0, sA0, sB0, sA2, sB2);
+  }
+  for (; ks < nks; ks += 4) {
+    step(ks, r0, r1, sA1, sB1, sA3, sB3);
+    if (ks + 1 < nks) step(ks + 1, r1, r0, sA2, sB2, sA0, sB0);
+    if (ks + 2 < nks) step(ks + 2, r0, r1, sA3, sB3, sA1, sB1);
+    if (ks + 3 < nks) step(ks + 3, r1, r0, sA0, sB0, sA2, sB2);
   }
   __syncthreads();
 
