@@ -25,10 +25,18 @@ import time
 import numpy as np
 
 METRIC = "BMLP train samples/s + XNOR-popcount MAC/s (% roofline), 4x4096 layers"
-# MI355X: 256 CUs x 4 SIMD16 = 64 lanes/CU-cycle at 2.4 GHz; one v_xor_b32 and
-# one v_bcnt_u32_b32 per 32 binary MACs; 1 MAC counted as 2 ops.
+# MI355X peaks (one binary MAC counted as 2 ops):
+# * popcount VALU: 256 CUs x 64 lanes x 2.4 GHz, one v_xor_b32 and one
+#   v_bcnt_u32_b32 per 32 binary MACs -> 6.29e14 MAC/s = 1258 TOP/s;
+# * dense MFMA: fp4 (e2m1) 10.1 PFLOP/s, int8 5.0 POP/s;
+# * HBM3E 8 TB/s.
 POPCOUNT_PEAK_TOPS = 256 * 64 * 2.4e9 * 32 / 2 * 2 / 1e12
+FP4_PEAK_TFLOPS = 10100.0
+INT8_PEAK_TOPS = 5000.0
 HBM_PEAK_GBS = 8000.0
+ROOT = os.path.dirname(os.path.abspath(__file__))
+FWD_SOURCES = {"fwd_fp4": "paper_2412_00119_amd/csrc/k_fwd_mfma.hip",
+               "fwd_popcount": "paper_2412_00119_amd/csrc/k_fwd_popcount.hip"}
 
 
 def log(*a):
@@ -40,6 +48,37 @@ def workload_macs(w, n):
     fwd = sum(n * w.widths[l] * w.widths[l - 1] for l in range(1, len(w.widths)))
     cls = sum(n * w.widths[l] * w.n_classes for l in range(1, len(w.widths)))
     return fwd, cls
+
+
+def update_bytes(w):
+    """Algorithmic HBM bytes of one update launch: H_l read and written, W_l
+    written as bit rows and as fp4 rows (all layers)."""
+    tot = 0
+    for l in range(1, len(w.widths)):
+        k_in, k_out = w.widths[l - 1], w.widths[l]
+        tot += 2 * k_out * k_in + k_out * 8 * ((k_in + 63) // 64) + k_out * 64 * ((k_in + 127) // 128)
+    return tot
+
+
+def source_sha256(rel):
+    import hashlib
+    with open(os.path.join(ROOT, rel), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed counter summary,
+    or None when there is none or the kernel source changed since."""
+    import re
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
+    m_b = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_sha or not m_b or m_sha.group(1) != source_sha256(FWD_SOURCES[kernel]):
+        return None
+    return float(m_b.group(1))
 
 
 def make_batches(w, torch, net, max_batches):
@@ -145,30 +184,67 @@ def main():
 
     run(args.warmup)
     torch.cuda.synchronize()
+    fwd_macs, cls_macs = workload_macs(w, w.batch)
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
-    ev0.record()
-    run(args.steps)
-    ev1.record()
-    torch.cuda.synchronize()
-    ms = ev0.elapsed_time(ev1)
+
+    def timed(k, profile):
+        """k steps between two events; with profile, every run of launches of
+        one kernel class is also bracketed by HIP events on the library's
+        stream (the stream the kernels are launched on)."""
+        torch.cuda.synchronize()
+        if profile:
+            B.bmlp_profile_start(net.ctx, k * (2 + 5 * w.n_layers) + 64)
+        ev0.record()
+        run(k)
+        ev1.record()
+        torch.cuda.synchronize()
+        prof = B.bmlp_profile_stop(net.ctx) if profile else None
+        return ev0.elapsed_time(ev1), prof
+
+    # The timed region: K steps.  Then the state is put back and the same K
+    # steps run again with per-kernel events (identical work: the update's
+    # cost follows the number of patterns in M, which falls as training goes).
+    saved, t_saved = net.state.clone(), t
+    ms, _ = timed(args.steps, False)
+    net.state.copy_(saved)
+    t = t_saved
+    ms_prof, prof = timed(args.steps, True)
+    del saved
     ms_step = ms / args.steps
     samples_s = args.steps * w.batch / (ms / 1e3)
-    fwd_macs, cls_macs = workload_macs(w, w.batch)
-    log(f"timed {args.steps} steps: {ms_step:.3f} ms/step, {samples_s:.4g} samples/s")
+    log(f"timed {args.steps} steps: {ms_step:.4f} ms/step, {samples_s:.4g} samples/s "
+        f"(same steps with per-kernel events: {ms_prof / args.steps:.4f} ms/step)")
+    kernels = {k: {"ms_per_step": v[0] / args.steps, "launches": v[1],
+                   "avg_launch_ms": v[0] / max(v[1], 1)} for k, v in prof.items()}
+    log("per-kernel ms/step: " + ", ".join(f"{k}={v['ms_per_step']:.4f}" for k, v in kernels.items()))
 
-    # Second pass over the same number of steps with every launch bracketed by
-    # HIP events on the library's stream: per-kernel-class durations.
-    per_step_launches = 2 + 5 * w.n_layers
-    B.bmlp_profile_start(net.ctx, args.steps * per_step_launches + 64)
-    run(args.steps)
-    prof = B.bmlp_profile_stop(net.ctx)
-    fwd_ms, fwd_n = prof["fwd"]
-    fwd_avg_ms = fwd_ms / max(fwd_n, 1)
+    # Roofline of the dominant kernel, the hidden-layer forward contraction:
+    # algorithmic binary MACs per launch (2 ops each) / average launch time.
+    mfma = args.fwd_impl in (0, 2)
+    fwd_avg_ms = kernels["fwd"]["avg_launch_ms"]
     macs_per_launch = fwd_macs / w.n_layers
     achieved = 2 * macs_per_launch / (fwd_avg_ms / 1e3) / 1e12
-    kernels = {k: {"ms_per_step": v[0] / args.steps, "launches": v[1]} for k, v in prof.items()}
-    log("per-kernel ms/step: " + ", ".join(f"{k}={v['ms_per_step']:.4f}" for k, v in kernels.items()))
+    kname = "fwd_fp4" if mfma else "fwd_popcount"
+    peak = FP4_PEAK_TFLOPS if mfma else POPCOUNT_PEAK_TOPS
+    traffic = measured_traffic(kname, w.name)
+    roofline = {"kernel": kname, "bound": "mfma" if mfma else "alu", "achieved": achieved,
+                "peak": peak, "unit": "TFLOP/s" if mfma else "TOP/s", "frac": achieved / peak,
+                "traffic": traffic, "avg_launch_ms": fwd_avg_ms,
+                "launches": kernels["fwd"]["launches"],
+                "algorithmic_ops_per_launch": 2 * macs_per_launch}
+    # the whole step's binary MAC rate against each compute roof, and the
+    # update kernel (the one full pass over H) against HBM
+    step_tops = 2 * (fwd_macs + cls_macs) / (ms_step / 1e3) / 1e12
+    upd = kernels["update"]
+    upd_gbs = update_bytes(w) / (upd["avg_launch_ms"] / 1e3) / 1e9 if upd["launches"] else None
+    step_roofline = {"ops_per_s_tera": step_tops,
+                     "frac_popcount_alu": step_tops / POPCOUNT_PEAK_TOPS,
+                     "frac_int8_mfma": step_tops / INT8_PEAK_TOPS,
+                     "frac_fp4_mfma": step_tops / FP4_PEAK_TFLOPS,
+                     "update_hbm_gbs": upd_gbs,
+                     "update_hbm_frac": upd_gbs / HBM_PEAK_GBS if upd_gbs else None,
+                     "update_bytes_per_launch": update_bytes(w)}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -184,6 +260,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_step,
+        "ms_per_step_with_kernel_events": ms_prof / args.steps,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -194,9 +271,8 @@ def main():
                    "robustness": w.robustness, "p_r": w.p_r, "parallelism": "single-gpu"},
         "mac_per_s": (fwd_macs + cls_macs) * args.steps / (ms / 1e3),
         "mac_per_step": fwd_macs + cls_macs,
-        "roofline": {"kernel": "fwd_popcount", "bound": "alu", "achieved": achieved,
-                     "peak": POPCOUNT_PEAK_TOPS, "unit": "TOP/s", "frac": achieved / POPCOUNT_PEAK_TOPS,
-                     "traffic": None, "avg_launch_ms": fwd_avg_ms, "launches": fwd_n},
+        "roofline": roofline,
+        "step_roofline": step_roofline,
         "kernels": kernels,
         "cpu_baseline": cpu,
     }

@@ -226,16 +226,20 @@ enum {
   BMLP_KERNEL_KINDS = 5
 };
 
-/* Profiling aid: brackets each of the next (at most max_launches) kernel
- * launches of this context with a pair of HIP events on the launch's
- * stream.  The events are host-created objects; no device buffer is
- * allocated.  Returns BMLP_EHIP if the events cannot be created. */
+/* Profiling aid: times the kernel launches of this context with HIP events
+ * on the launch's stream.  Consecutive launches of one kernel class on one
+ * stream within one API call form a run that shares a single pair of events
+ * (so the event overhead is paid once per run); at most max_launches runs
+ * are recorded, later launches go untimed.  The events are host-created
+ * objects; no device buffer is allocated.  Returns BMLP_EHIP if the events
+ * cannot be created. */
 int bmlp_profile_start(bmlp_ctx *ctx, int32_t max_launches);
 
 /* Ends profiling: waits for the last recorded event, then writes per kernel
- * class the summed duration in milliseconds (h_ms[BMLP_KERNEL_KINDS]) and the
- * number of timed launches (h_launches[BMLP_KERNEL_KINDS]), and releases the
- * events.  Either output may be NULL. */
+ * class the summed duration of its runs in milliseconds
+ * (h_ms[BMLP_KERNEL_KINDS]) and the number of launches in those runs
+ * (h_launches[BMLP_KERNEL_KINDS]), and releases the events.  Either output
+ * may be NULL. */
 int bmlp_profile_stop(bmlp_ctx *ctx, double *h_ms, int64_t *h_launches);
 
 /* Frees the host-side context.  Device buffers stay with the caller. */

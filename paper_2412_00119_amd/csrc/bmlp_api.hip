@@ -10,8 +10,11 @@
 #include "bmlp_internal.h"
 #include "fp4.h"
 
+// One run of consecutive launches of one kernel class on one stream, within
+// one API call, bracketed by a single pair of events.
 struct ProfRec {
   int kind;
+  int launches;
   hipEvent_t t0, t1;
 };
 
@@ -21,6 +24,8 @@ struct bmlp_ctx {
   uint8_t *ws;
   bool prof_on = false;
   size_t prof_used = 0;
+  long prof_open = -1;          // index of the run still open, or -1
+  hipStream_t prof_stream = nullptr;
   std::vector<ProfRec> prof;
 };
 
@@ -40,21 +45,45 @@ int hip_fail(hipError_t e, const char *where) {
     if (e_ != hipSuccess) return hip_fail(e_, #call);        \
   } while (0)
 
-// Launch with optional event bracketing (profiling aid).
+// Ends the open profiling run (if any) with its closing event.
+inline hipError_t prof_close(bmlp_ctx *ctx) {
+  if (ctx->prof_open < 0) return hipSuccess;
+  const hipError_t e = hipEventRecord(ctx->prof[ctx->prof_open].t1, ctx->prof_stream);
+  ctx->prof_open = -1;
+  return e;
+}
+
+// Closes the open profiling run when an API call returns, so that no run
+// spans host time between calls.
+struct ProfScope {
+  bmlp_ctx *ctx;
+  ~ProfScope() {
+    if (ctx != nullptr) (void)prof_close(ctx);
+  }
+};
+
+// Launch with optional event bracketing (profiling aid): a launch of another
+// class or on another stream closes the open run and opens a new one.
 #define BMLP_TIMED(ctx, kind_, s, call)                                         \
   do {                                                                         \
-    ProfRec *r_ = nullptr;                                                     \
-    if ((ctx)->prof_on && (ctx)->prof_used < (ctx)->prof.size()) {             \
-      r_ = &(ctx)->prof[(ctx)->prof_used++];                                   \
-      r_->kind = (kind_);                                                      \
-      hipError_t ee_ = hipEventRecord(r_->t0, (s));                            \
-      if (ee_ != hipSuccess) return hip_fail(ee_, "hipEventRecord");           \
+    if ((ctx)->prof_on) {                                                      \
+      if ((ctx)->prof_open >= 0 &&                                             \
+          ((ctx)->prof[(ctx)->prof_open].kind != (kind_) || (ctx)->prof_stream != (s))) { \
+        hipError_t ee_ = prof_close(ctx);                                      \
+        if (ee_ != hipSuccess) return hip_fail(ee_, "hipEventRecord");         \
+      }                                                                        \
+      if ((ctx)->prof_open < 0 && (ctx)->prof_used < (ctx)->prof.size()) {     \
+        ProfRec &r_ = (ctx)->prof[(ctx)->prof_used];                           \
+        r_.kind = (kind_);                                                     \
+        r_.launches = 0;                                                       \
+        hipError_t ee_ = hipEventRecord(r_.t0, (s));                           \
+        if (ee_ != hipSuccess) return hip_fail(ee_, "hipEventRecord");         \
+        (ctx)->prof_open = (long)(ctx)->prof_used++;                           \
+        (ctx)->prof_stream = (s);                                              \
+      }                                                                        \
     }                                                                          \
     BMLP_LAUNCH(call);                                                         \
-    if (r_ != nullptr) {                                                       \
-      hipError_t ee_ = hipEventRecord(r_->t1, (s));                            \
-      if (ee_ != hipSuccess) return hip_fail(ee_, "hipEventRecord");           \
-    }                                                                          \
+    if ((ctx)->prof_on && (ctx)->prof_open >= 0) (ctx)->prof[(ctx)->prof_open].launches++; \
   } while (0)
 
 inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
@@ -177,6 +206,7 @@ bool use_mfma(const Plan &p) { return p.fwd_impl != BMLP_FWD_POPCOUNT; }
 // Forward of every layer for inference (y_hat out) or evaluation (counts).
 int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32_t *yhat_out,
                    const int32_t *y, int32_t *correct) {
+  ProfScope prof_scope{ctx};
   const Plan &p = ctx->plan;
   int32_t *yh_ws = reinterpret_cast<int32_t *>(ctx->ws + p.off_yhat);
   if (use_mfma(p)) {
@@ -372,6 +402,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
   const Plan &p = ctx->plan;
   hipStream_t s = as_stream(stream);
   const bool mfma = use_mfma(p);
+  ProfScope prof_scope{ctx};
   if (n == 0 || !mfma)
     BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s, launch_fill_i32(d_stats, 4 * p.L, 0, s));
   if (n == 0) return BMLP_OK;
@@ -520,6 +551,7 @@ static void prof_release(bmlp_ctx *ctx) {
   }
   ctx->prof.clear();
   ctx->prof_used = 0;
+  ctx->prof_open = -1;
   ctx->prof_on = false;
 }
 
@@ -527,7 +559,7 @@ int bmlp_profile_start(bmlp_ctx *ctx, int32_t max_launches) {
   if (ctx == nullptr) return BMLP_EINVAL;
   if (max_launches < 1 || max_launches > (1 << 20)) return BMLP_ESHAPE;
   prof_release(ctx);
-  ctx->prof.resize((size_t)max_launches, ProfRec{0, nullptr, nullptr});
+  ctx->prof.resize((size_t)max_launches, ProfRec{0, 0, nullptr, nullptr});
   for (ProfRec &r : ctx->prof) {
     hipError_t e = hipEventCreate(&r.t0);
     if (e == hipSuccess) e = hipEventCreate(&r.t1);
@@ -545,7 +577,11 @@ int bmlp_profile_stop(bmlp_ctx *ctx, double *h_ms, int64_t *h_launches) {
   double ms[BMLP_KERNEL_KINDS] = {0};
   int64_t cnt[BMLP_KERNEL_KINDS] = {0};
   int status = BMLP_OK;
-  if (ctx->prof_used > 0) {
+  if (ctx->prof_open >= 0) {
+    const hipError_t e = prof_close(ctx);
+    if (e != hipSuccess) status = hip_fail(e, "hipEventRecord");
+  }
+  if (status == BMLP_OK && ctx->prof_used > 0) {
     hipError_t e = hipEventSynchronize(ctx->prof[ctx->prof_used - 1].t1);
     if (e != hipSuccess) status = hip_fail(e, "hipEventSynchronize");
     for (size_t i = 0; status == BMLP_OK && i < ctx->prof_used; ++i) {
@@ -556,7 +592,7 @@ int bmlp_profile_stop(bmlp_ctx *ctx, double *h_ms, int64_t *h_launches) {
         break;
       }
       ms[ctx->prof[i].kind] += t;
-      cnt[ctx->prof[i].kind] += 1;
+      cnt[ctx->prof[i].kind] += ctx->prof[i].launches;
     }
   }
   prof_release(ctx);
