@@ -137,6 +137,17 @@ def stream_bits(seed: int, layer: int, stream: int, j: np.ndarray, t: int = 0) -
     return ((w >> (b & 31).astype(np.uint32)) & np.uint32(1)).astype(np.uint8)
 
 
+def stream_bits_prefix(seed: int, layer: int, stream: int, n: int, t: int = 0) -> np.ndarray:
+    """stream_bits for j = 0..n-1, written as the layout itself: the 128
+    output bits of block q (four words, each LSB first) are elements
+    128q .. 128q+127."""
+    k0, k1 = philox_key(seed)
+    nb = (int(n) + 127) // 128
+    words = np.stack(philox4x32_10(np.arange(nb, dtype=np.uint64), layer - 1, t & MASK32, stream, k0, k1),
+                     axis=-1).astype("<u4")
+    return np.unpackbits(words.view(np.uint8).reshape(-1), bitorder="little")[:n]
+
+
 def reinforce_draws(seed: int, layer: int, t: int, j: np.ndarray) -> np.ndarray:
     """The 32-bit uniform draw u = u8 * 2^24 + u24 of each flat index j."""
     j = np.asarray(j, dtype=np.uint64)
@@ -212,8 +223,8 @@ class State:
 def init_layer(cfg: Config, l: int):
     """H_l and P_l uniform on {-1, +1} (Algorithm 1, initialisation; R9)."""
     kin, kout, c = cfg.widths[l - 1], cfg.widths[l], cfg.n_classes
-    hb = stream_bits(cfg.seed, l, STREAM_H_INIT, np.arange(kin * kout, dtype=np.uint64))
-    pb = stream_bits(cfg.seed, l, STREAM_P_INIT, np.arange(c * kout, dtype=np.uint64))
+    hb = stream_bits_prefix(cfg.seed, l, STREAM_H_INIT, kin * kout)
+    pb = stream_bits_prefix(cfg.seed, l, STREAM_P_INIT, c * kout)
     H = np.where(hb == 1, 1, -1).astype(np.int8).reshape(kout, kin)
     P = np.where(pb == 1, 1, -1).astype(np.int8).reshape(c, kout)
     return H, P

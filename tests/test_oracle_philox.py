@@ -83,6 +83,14 @@ def test_init_bits_layout():
     np.testing.assert_array_equal(ob.stream_bits(42, 3, ob.STREAM_H_INIT, idx), expect[idx.astype(int)])
 
 
+@pytest.mark.parametrize("n", [1, 127, 128, 129, 1000, 4096 + 5])
+def test_prefix_bits_match_gathered_bits(n):
+    """The whole-range form used at init equals the per-index form."""
+    for stream in (ob.STREAM_H_INIT, ob.STREAM_P_INIT):
+        np.testing.assert_array_equal(ob.stream_bits_prefix(0x1234_5678_9ABC, 2, stream, n),
+                                      ob.stream_bits(0x1234_5678_9ABC, 2, stream, np.arange(n, dtype=np.uint64)))
+
+
 def test_reinforce_draws_layout():
     j = np.arange(64, dtype=np.uint64)
     u = ob.reinforce_draws(7, 2, 5, j)
