@@ -74,7 +74,7 @@ enum { kFwdFusedSelect = 0, kFwdWriteZ = 1, kFwdPlain = 2 };
 struct FwdArgs {
   const uint8_t *A; int lda;        // a_{l-1} fp4 [M][lda]
   const uint8_t *B; int ldb;        // W_l fp4 [N][ldb]
-  int M, N, ksteps;                 // ksteps = lda / 64
+  int M, N, ksteps;                 // ksteps = lda / 64 (>= 1)
   uint64_t *abits; int words_out;   // a_l bits [M][words_out]
   uint8_t *afp4; int ld_af;         // a_l fp4 [M][ld_af]
   int mode;
@@ -82,6 +82,7 @@ struct FwdArgs {
   const int32_t *y; const uint64_t *Pbits; int c;
   int16_t *z; int ldz;              // kFwdWriteZ
   int nt_m, nt_n, xcd_remap;        // set by the launcher
+  int ldp, pw_max;                  // set by the launcher: Pbits row stride and last word
 };
 hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s);
 

@@ -9,9 +9,10 @@
 // four waves of 64 x 64; K is walked in steps of 128 elements through a
 // ring of kStages LDS buffers filled by direct-to-LDS loads
 // (global_load_lds_dwordx4) three steps ahead of the matrix cores, with one
-// barrier per step; operands are read from LDS one step ahead.  Rows past the matrix end are clamped into range:
-// they only feed outputs that are never stored.  The epilogue never writes z
-// to memory:
+// barrier per step; operands are read from LDS one step ahead, in between
+// the MFMAs.  Rows past the matrix end are clamped into range: they only
+// feed outputs that are never stored.  The epilogue never writes z to
+// memory:
 //   * a_l as bit rows (wave ballots) and as fp4 rows for the next layer and
 //     the classifier;
 //   * for gamma = 64, the easiest wrong perceptron of each group: among the
@@ -32,7 +33,7 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 
 constexpr int TM = 128, TN = 128;   // tile of z
 constexpr int KB = 64;              // bytes per row per K step (128 fp4)
-constexpr int kStages = 4;          // LDS ring depth
+constexpr int kStages = 4;          // LDS ring depth (kStages - 1 steps in flight)
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -44,8 +45,10 @@ __device__ __forceinline__ void dma16(const void *src, void *dst_wave_base) {
 // wait until at most n vector-memory operations of this wave are outstanding
 template <int N>
 __device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N < 16, "vmcnt field");
-  __builtin_amdgcn_s_waitcnt(0xF70 | N);   // expcnt and lgkmcnt left unconstrained
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  // vmcnt in bits 3:0 and 15:14; expcnt (6:4) and lgkmcnt (11:8) at their
+  // maxima, i.e. not waited for
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0xF70);
 }
 
 // XOR swizzle of the 16-byte chunk index within a 64-byte LDS row.  LDS has
@@ -69,11 +72,12 @@ __device__ __forceinline__ v16f mfma_fp4(const uint4 &a, const uint4 &b, v16f c)
 }
 
 __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
-  // one LDS array per ring slot and operand: every access below names its
-  // array, so the compiler can tell a slot being read from the slots the
-  // direct-to-LDS loads are still filling
-  __shared__ __align__(16) uint8_t sA0[TM * KB], sA1[TM * KB], sA2[TM * KB], sA3[TM * KB];
-  __shared__ __align__(16) uint8_t sB0[TN * KB], sB1[TN * KB], sB2[TN * KB], sB3[TN * KB];
+  // one LDS array per ring slot (A tile, then B tile): every access below
+  // names its array, so the compiler can tell a slot being read from the
+  // slots the direct-to-LDS loads are still filling (it tells apart at most
+  // eight such arrays).  66 KB in all: two work-groups fit on a CU.
+  constexpr int kSlot = (TM + TN) * KB;
+  __shared__ __align__(16) uint8_t s0[kSlot], s1[kSlot], s2[kSlot], s3[kSlot];
   __shared__ uint64_t sP[TM][2];       // rho^{y^mu} bits of the tile's 128 columns
   static_assert(kStages == 4, "one named array per slot");
 
@@ -93,18 +97,18 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   }
   const int m0 = mt * TM, n0 = nt * TN;
 
-  if (p.mode == kFwdFusedSelect) {
-    // the classifier row of each pattern's label, for the tile's columns
-    const int r = tid >> 1, w = tid & 1;
-    const int m = m0 + r;
-    const int wg = (n0 >> 6) + w;
-    uint64_t v = 0;
-    if (m < p.M && wg < p.words_out) {
-      const int yl = min(max(p.y[m], 0), p.c - 1);
-      v = p.Pbits[(size_t)yl * p.words_out + wg];
-    }
-    sP[r][w] = v;
-  }
+  // For the fused selection: thread (r, w) fetches word w of the tile's
+  // columns of rho^{y^mu} for tile row r (pattern m0 + r), before the
+  // operand loads start (the compiler does not count direct-to-LDS loads, so
+  // a register load issued among them would make it wait for all of them).
+  // The loads are unconditional (indices clamped; when the selection is not
+  // fused the launcher points them at valid memory with a zero row stride).
+  const int pr = tid >> 1, pw = tid & 1;
+  const int pm = m0 + pr, pwg = (n0 >> 6) + pw;
+  const bool pvalid = p.mode == kFwdFusedSelect && pm < p.M && pwg < p.words_out;
+  const int yl = min(max(p.y[min(pm, p.M - 1)], 0), p.c - 1);
+  const uint64_t prow = p.Pbits[(size_t)yl * p.ldp + min(pwg, p.pw_max)];
+  __builtin_amdgcn_sched_barrier(0);
 
   // Loads: a wave moves rows 32*wave .. 32*wave+31 of each operand, 16 rows
   // (1 KB) per instruction; lane l fills LDS bytes 16*l of the 1 KB, i.e. row
@@ -118,11 +122,11 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     srcA[h] = p.A + (size_t)min(m0 + r, p.M - 1) * p.lda + c * 16;
     srcB[h] = p.B + (size_t)min(n0 + r, p.N - 1) * p.ldb + c * 16;
   }
-  auto issue = [&](int ks, uint8_t *dA, uint8_t *dB) {
+  auto issue = [&](int ks, uint8_t *d) {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      dma16(srcA[h] + ks * KB, dA + (2 * wave + h) * 1024);
-      dma16(srcB[h] + ks * KB, dB + (2 * wave + h) * 1024);
+      dma16(srcA[h] + ks * KB, d + (2 * wave + h) * 1024);
+      dma16(srcB[h] + ks * KB, d + TM * KB + (2 * wave + h) * 1024);
     }
   };
 
@@ -137,7 +141,8 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     uint4 a[2][2], b[2][2];
   };
   const int arow = lane & 31, ahalf = lane >> 5;
-  auto read = [&](Ops &o, const uint8_t *tA, const uint8_t *tB) {
+  auto read = [&](Ops &o, const uint8_t *t) {
+    const uint8_t *tA = t, *tB = t + TM * KB;
 #pragma unroll
     for (int kh = 0; kh < 2; ++kh) {
       const int ch = 2 * kh + ahalf;   // 16-byte chunk of the 64-byte K step
@@ -160,80 +165,67 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
 
   // Pipeline of step ks: the loads of step ks+3 are issued into the slot of
   // step ks-1, the MFMAs of step ks run on operands read during step ks-1,
-  // and then the operands of step ks+1 are read from LDS (after the MFMAs in
-  // program order, so the reads complete under them and the next barrier).
-  // The slot of step ks-1 is free: its operands fed MFMAs issued before this
-  // step's barrier.
+  // and the operands of step ks+1 are read from LDS in between the MFMAs, so
+  // the reads complete under them.  The slot of step ks-1 is free: its
+  // operands fed MFMAs issued before this step's barrier.
+  //
+  // Every step issues its loads, of step min(ks+3, nks-1): past the end they
+  // repeat the last step into slots nobody reads.  So the count of loads in
+  // flight is the same at every step and the code has no branches for the
+  // compiler's wait-count tracking to merge over (a merge makes it wait for
+  // every load before the next LDS read).
   const int nks = p.ksteps;
-  if (0 < nks) issue(0, sA0, sB0);
-  if (1 < nks) issue(1, sA1, sB1);
-  if (2 < nks) issue(2, sA2, sB2);
-  // this wave's loads of step t are done when at most 4 * (steps issued
-  // after t) loads are in flight
-  auto wait_step = [&](int t, int issued_last) {
-    const int after = min(2, issued_last - t);
-    if (after >= 2)
-      wait_vm<8>();
-    else if (after == 1)
-      wait_vm<4>();
-    else
-      wait_vm<0>();
-  };
+  const int klast = nks - 1;   // nks >= 1
+  issue(0, s0);
+  issue(min(1, klast), s1);
+  issue(min(2, klast), s2);
+  __builtin_amdgcn_sched_barrier(0);
   Ops r0, r1;
-  if (0 < nks) {
-    wait_step(0, min(2, nks - 1));
-    __builtin_amdgcn_s_barrier();   // every wave's loads of step 0 have landed
-    read(r0, sA0, sB0);
-  }
-  // one step with every bound checked (used for the last few steps)
-  auto step = [&](int ks, Ops &cur, Ops &nxt, const uint8_t *rA, const uint8_t *rB, uint8_t *dA,
-                  uint8_t *dB) {
-    if (ks + 1 < nks) {
-      wait_step(ks + 1, min(ks + 2, nks - 1));
-      // A plain s_barrier: the fence of __syncthreads would also wait for
-      // the loads still in flight for later steps.
-      __builtin_amdgcn_s_barrier();
-      if (ks + 3 < nks) issue(ks + 3, dA, dB);
-    }
-    compute(cur);
-    __builtin_amdgcn_sched_barrier(0);   // keep the reads below the MFMAs
-    if (ks + 1 < nks) read(nxt, rA, rB);
-  };
-  // the same step in the steady state (steps ks+1..ks+3 exist): no branches,
-  // so the compiler can count the LDS reads in flight
+  wait_vm<4 * (kStages - 2)>();   // this wave's loads of step 0 are done
+  __builtin_amdgcn_s_barrier();    // every wave's loads of step 0 have landed
+  read(r0, s0);
+  __builtin_amdgcn_sched_barrier(0);
   // The sched_barrier(0) fences pin the order of the phases; otherwise the
   // scheduler sinks the read-ahead to its use and the LDS latency reappears.
-  auto step_full = [&](int ks, Ops &cur, Ops &nxt, const uint8_t *rA, const uint8_t *rB, uint8_t *dA,
-                       uint8_t *dB) {
+  auto step = [&](int ks, Ops &cur, Ops &nxt, const uint8_t *rs, uint8_t *ds) {
     __builtin_amdgcn_sched_barrier(0);
-    wait_vm<4>();   // step ks+1 landed; step ks+2 may still be in flight
+    wait_vm<4 * (kStages - 3)>();   // step ks+1 landed; ks+2 may still be in flight
+    // A plain s_barrier: the fence of __syncthreads would also wait for the
+    // loads still in flight for later steps.
     __builtin_amdgcn_s_barrier();
-    issue(ks + 3, dA, dB);
+    issue(min(ks + kStages - 1, klast), ds);
     __builtin_amdgcn_sched_barrier(0);
     compute(cur);
-    __builtin_amdgcn_sched_barrier(0);
-    read(nxt, rA, rB);
+    read(nxt, rs);   // past the last step this reads a slot nobody uses
+    // one LDS read after each MFMA
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+    }
     __builtin_amdgcn_sched_barrier(0);
   };
+  // step ks reads slot (ks+1) % 4 and refills slot (ks+3) % 4
   int ks = 0;
-  for (; ks + 7 <= nks; ks += 4) {
-    step_full(ks, r0, r1, sA1, sB1, sA3, sB3);
-    step_full(ks + 1, r1, r0, sA2, sB2, sA0, sB0);
-    step_full(ks + 2, r0, r1, sA3, sB3, sA1, sB1);
-    step_full(ks + 3, r1, r0, sA0, sB0, sA2, sB2);
+  for (; ks + kStages <= nks; ks += kStages) {
+    step(ks + 0, r0, r1, s1, s3);
+    step(ks + 1, r1, r0, s2, s0);
+    step(ks + 2, r0, r1, s3, s1);
+    step(ks + 3, r1, r0, s0, s2);
   }
-  for (; ks < nks; ks += 4) {
-    step(ks, r0, r1, sA1, sB1, sA3, sB3);
-    if (ks + 1 < nks) step(ks + 1, r1, r0, sA2, sB2, sA0, sB0);
-    if (ks + 2 < nks) step(ks + 2, r0, r1, sA3, sB3, sA1, sB1);
-    if (ks + 3 < nks) step(ks + 3, r1, r0, sA0, sB0, sA2, sB2);
+  if (ks < nks) {   // the last nks % 4 steps
+    step(ks + 0, r0, r1, s1, s3);
+    if (ks + 1 < nks) step(ks + 1, r1, r0, s2, s0);
+    if (ks + 2 < nks) step(ks + 2, r0, r1, s3, s1);
   }
+  wait_vm<0>();   // the repeated loads of the last steps have landed
+  sP[pr][pw] = pvalid ? prow : 0ull;
   __syncthreads();
 
   // ---- epilogue ---------------------------------------------------------------
   // lane holds z for column n0 + wn*64 + j*32 + (lane & 31) and rows
   // m0 + wm*64 + i*32 + 8*(e >> 2) + 4*(lane >> 5) + (e & 3) in acc[i][j][e]
-  uint32_t *sbits = reinterpret_cast<uint32_t *>(sA0);   // [128 rows][4 chunks of 32 columns]
+  uint32_t *sbits = reinterpret_cast<uint32_t *>(s0);   // [128 rows][4 chunks of 32 columns]
   const int lh = lane >> 5, lc = lane & 31;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -367,6 +359,16 @@ hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s) {
   a.nt_m = (a.M + TM - 1) / TM;
   a.nt_n = (a.N + TN - 1) / TN;
   a.xcd_remap = (a.nt_n % 8 == 0) ? 1 : 0;
+  if (a.mode == kFwdFusedSelect) {
+    a.ldp = a.words_out;
+    a.pw_max = a.words_out - 1;
+  } else {   // the kernel's label / classifier loads read A instead (always valid)
+    a.y = reinterpret_cast<const int32_t *>(a.A);
+    a.Pbits = reinterpret_cast<const uint64_t *>(a.A);
+    a.c = 1;
+    a.ldp = 0;
+    a.pw_max = 0;
+  }
   hipLaunchKernelGGL(fwd_fp4_kernel, dim3(a.nt_m * a.nt_n), dim3(256), 0, s, a);
   return hipGetLastError();
 }
