@@ -104,14 +104,22 @@ typedef struct bmlp_config {
  *   k_in, k_out      K_{l-1}, K_l.
  *   gamma, groups    group size and G_l = K_l / gamma.
  *   words_in/out     uint64 words per bit row of a_{l-1} / a_l.
- *   ld_h             bytes per row of H_l (>= k_in, a multiple of 64).
+ *   ld_h             bytes per row of H_l (one byte per column, >= k_in,
+ *                    a multiple of 64).
  *   robust_thr       ceil(r * K_l), computed in IEEE double.
  *   ldq_in/out       bytes per fp4 row of K_{l-1} / K_l values (64 per 128 values).
  *   off_h, off_w, off_p  byte offsets in the state buffer of
- *                    H_l  int8   [k_out][ld_h]       hidden weights, perceptron-major
+ *                    H_l  [k_out][ld_h bytes]  int8 hidden weights, perceptron-major
  *                                                    (the transpose of the paper's
- *                                                    K_{l-1} x K_l, so h^k is a row);
- *                                                    bytes past k_in in a row are 0;
+ *                                                    K_{l-1} x K_l, so h^k is a row),
+ *                                                    stored bit-sliced: columns
+ *                                                    32g .. 32g+31 of a row are the
+ *                                                    32 bytes at 32g, read as eight
+ *                                                    uint32 words; bit i of word p
+ *                                                    is bit p of the two's-complement
+ *                                                    value of column 32g + i.
+ *                                                    Columns past k_in hold 0.
+ *                                                    bmlp_read_h unpacks it;
  *                    W_l  uint64 [k_out][words_in]   visible weights sign(H_l), bits;
  *                    P_l  uint64 [n_classes][words_out]  fixed classifier, row y is rho^y;
  *                    and, as matrix-core operands, copies of W_l (off_wq, uint8
@@ -202,8 +210,14 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
 int bmlp_eval(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int32_t n,
               int32_t *d_correct, void *stream);
 
-/* Device pointers to H_l, W_l and P_l of layer l (1..L) in the state. */
-int bmlp_layer_views(bmlp_ctx *ctx, int32_t l, int8_t **d_h, uint64_t **d_w, uint64_t **d_p);
+/* Device pointers to H_l (bit-sliced, see bmlp_layer_info), W_l and P_l of
+ * layer l (1..L) in the state. */
+int bmlp_layer_views(bmlp_ctx *ctx, int32_t l, uint8_t **d_h, uint64_t **d_w, uint64_t **d_p);
+
+/* Unpacks the hidden weights of layer l (1..L) into plain int8
+ * d_out[k_out][k_in] (caller-owned, k_out * k_in bytes), asynchronously on
+ * stream.  For checkpoints in a portable form and for inspection. */
+int bmlp_read_h(bmlp_ctx *ctx, int32_t l, int8_t *d_out, void *stream);
 
 /* Device pointers to the last train step's per-layer trace in the workspace
  * (layouts in bmlp_layer_info).  bmlp_forward and bmlp_eval overwrite a_l. */

@@ -45,12 +45,13 @@ Random numbers come from Philox4x32-10 (``oracle.philox``) keyed by the
   stream 1  H init: bit (j & 127) of the 128 output bits of block j >> 7,
             j = k*K_{l-1} + i (word b >> 5, bit b & 31 with b = j & 127).
   stream 2  P init: same, j = class*K_l + k.
-  stream 3  reinforcement, coarse byte: u8 = byte (j & 3) of word
-            ((j & 15) >> 2) of block j >> 4.
+  stream 3  reinforcement, coarse byte of hidden weight (k, i): with
+            q = k * ceil(K_{l-1} / 32) + (i >> 5) (the row's 32-column group),
+            bit p of u8 is bit (i & 31) of word p & 3 of block 2q + (p >> 2).
   stream 4  reinforcement, fine bits: u24 = low 24 bits of word (j & 3) of
-            block j >> 2.
-  The 32-bit draw of hidden weight j is u = u8 * 2^24 + u24; it reinforces
-  when u < T_l.  Init uses t = 0.
+            block j >> 2, j = k * K_{l-1} + i.
+  The 32-bit draw of hidden weight (k, i) is u = u8 * 2^24 + u24; it
+  reinforces when u < T_l.  Init uses t = 0.
 """
 from __future__ import annotations
 
@@ -148,27 +149,37 @@ def stream_bits_prefix(seed: int, layer: int, stream: int, n: int, t: int = 0) -
     return np.unpackbits(words.view(np.uint8).reshape(-1), bitorder="little")[:n]
 
 
-def reinforce_draws(seed: int, layer: int, t: int, j: np.ndarray) -> np.ndarray:
-    """The 32-bit uniform draw u = u8 * 2^24 + u24 of each flat index j."""
+def reinforce_draws(seed: int, layer: int, t: int, j: np.ndarray, k_in: int) -> np.ndarray:
+    """The 32-bit uniform draw u = u8 * 2^24 + u24 of each flat index
+    j = k * K_{l-1} + i of a layer with K_{l-1} = k_in inputs."""
     j = np.asarray(j, dtype=np.uint64)
-    # coarse byte: stream 3, 16 bytes per block
-    cw, inv = _blocks(seed, layer, t, STREAM_R_COARSE, j >> np.uint64(4))
-    jj = (j & np.uint64(15)).astype(np.int64)
-    word = cw[inv, jj >> 2]
-    u8 = (word >> (8 * (jj & 3)).astype(np.uint32)) & np.uint32(0xFF)
+    kin = np.uint64(k_in)
+    k, i = j // kin, j % kin
+    # coarse byte: stream 3, eight words (two blocks) per 32-column group,
+    # word p giving bit p of the 32 bytes
+    q = k * np.uint64((k_in + 31) // 32) + (i >> np.uint64(5))
+    b2 = q * np.uint64(2)
+    words, inv = _blocks(seed, layer, t, STREAM_R_COARSE, np.concatenate([b2, b2 + np.uint64(1)]))
+    m = j.size
+    planes = np.concatenate([words[inv[:m]], words[inv[m:]]], axis=1)   # [len(j)][8]
+    bit = (i & np.uint64(31)).astype(np.uint32)
+    u8 = np.zeros(j.shape, dtype=np.uint32)
+    for p in range(8):
+        u8 |= ((planes[:, p] >> bit) & np.uint32(1)) << np.uint32(p)
     # fine bits: stream 4, four 24-bit values per block
     fw, inv = _blocks(seed, layer, t, STREAM_R_FINE, j >> np.uint64(2))
     u24 = fw[inv, (j & np.uint64(3)).astype(np.int64)] & np.uint32(0xFFFFFF)
     return (u8.astype(np.uint64) << np.uint64(24)) | u24.astype(np.uint64)
 
 
-def reinforce_mask(seed: int, layer: int, t: int, thresh: int, n: int,
+def reinforce_mask(seed: int, layer: int, t: int, thresh: int, n: int, k_in: int,
                    chunk: int = 1 << 22) -> np.ndarray:
-    """Bernoulli(T / 2^32) draws for flat indices 0..n-1: u < T (R12)."""
+    """Bernoulli(T / 2^32) draws for flat indices 0..n-1 of a layer with
+    K_{l-1} = k_in: u < T (R12)."""
     out = np.empty(n, dtype=bool)
     for s in range(0, n, chunk):
         e = min(n, s + chunk)
-        u = reinforce_draws(seed, layer, t, np.arange(s, e, dtype=np.uint64))
+        u = reinforce_draws(seed, layer, t, np.arange(s, e, dtype=np.uint64), k_in)
         out[s:e] = u < np.uint64(thresh)
     return out
 
@@ -364,7 +375,7 @@ def train_step(state: State, x: np.ndarray, y: np.ndarray, t: int, p_r: float,
             # LayerUpdate / PerceptronUpdate run only when M_l is not empty.
             S = selection_matrix(kstar, P, y, gamma)
             h1 = clip(H.astype(np.int64) + cp_increment(S, a_prev), cfg.bound)
-            mask = reinforce_mask(cfg.seed, l, t, reinforce_threshold(p_r, kout), kin * kout)
+            mask = reinforce_mask(cfg.seed, l, t, reinforce_threshold(p_r, kout), kin * kout, kin)
             nreinf = int(mask.sum())
             state.H[l - 1] = reinforce(h1, mask, cfg.bound).astype(np.int8)
         traces.append(LayerTrace(a, z, yhat, pred, tau, err, upd, kstar,

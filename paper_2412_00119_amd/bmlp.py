@@ -92,6 +92,7 @@ def lib() -> ctypes.CDLL:
                                                 ctypes.POINTER(vp)]),
             "bmlp_step_trace": (ctypes.c_int, [vp, i32, ctypes.POINTER(vp), ctypes.POINTER(vp),
                                                ctypes.POINTER(vp), ctypes.POINTER(vp)]),
+            "bmlp_read_h": (ctypes.c_int, [vp, i32, vp, vp]),
             "bmlp_status_string": (ctypes.c_char_p, [ctypes.c_int]),
             "bmlp_last_error": (ctypes.c_char_p, []),
             "bmlp_destroy": (None, [vp]),
@@ -181,6 +182,10 @@ def bmlp_train_step(ctx: int, d_x: int, d_y: int, n: int, step: int, p_r: float,
 
 def bmlp_eval(ctx: int, d_x: int, d_y: int, n: int, d_correct: int, stream: int):
     _check(lib().bmlp_eval(ctx, d_x, d_y, n, d_correct, stream), "bmlp_eval")
+
+
+def bmlp_read_h(ctx: int, layer: int, d_out: int, stream: int):
+    _check(lib().bmlp_read_h(ctx, layer, d_out, stream), "bmlp_read_h")
 
 
 def bmlp_destroy(ctx: int):
@@ -307,10 +312,17 @@ class BMLP:
         return buf[off:off + nbytes].view(dtype).view(*shape)
 
     def H(self, l: int):
-        """Hidden weights of layer l, int8 [K_l][K_{l-1}] (a view into the state)."""
+        """Hidden weights of layer l unpacked to int8 [K_l][K_{l-1}] (a new tensor;
+        the state keeps them bit-sliced, see H_planes)."""
         i = self.info[l - 1]
-        full = self._view(self.state, i.off_h, i.k_out * i.ld_h, self.torch.int8, (i.k_out, i.ld_h))
-        return full[:, :i.k_in]
+        out = self.torch.empty((i.k_out, i.k_in), dtype=self.torch.int8, device=self.device)
+        bmlp_read_h(self.ctx, l, out.data_ptr(), self._stream())
+        return out
+
+    def H_planes(self, l: int):
+        """The state's bit-sliced hidden weights of layer l, uint8 [K_l][ld_h]."""
+        i = self.info[l - 1]
+        return self._view(self.state, i.off_h, i.k_out * i.ld_h, self.torch.uint8, (i.k_out, i.ld_h))
 
     def W(self, l: int):
         i = self.info[l - 1]

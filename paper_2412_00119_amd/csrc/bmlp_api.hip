@@ -288,7 +288,7 @@ int setup(const bmlp_config *cfg, void *d_state, void *d_ws, void *stream, bmlp_
   hipStream_t s = as_stream(stream);
   for (int l = 1; l <= p.L; ++l) {
     const LayerPlan &lp = p.layer[l - 1];
-    int8_t *H = reinterpret_cast<int8_t *>(ctx->state + lp.off_h);
+    uint8_t *H = ctx->state + lp.off_h;
     uint64_t *W = reinterpret_cast<uint64_t *>(ctx->state + lp.off_w);
     uint64_t *P = reinterpret_cast<uint64_t *>(ctx->state + lp.off_p);
     hipError_t e = launch_init_h(H, lp.ld_h, W, lp.words_in, lp.k_in, lp.k_out, p.seed, l, from_h, s);
@@ -487,7 +487,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
   for (int l = 1; l <= p.L; ++l) {
     const LayerPlan &lp = p.layer[l - 1];
     UpdLayer &u = ub.L[ub.nl++];
-    u.H = reinterpret_cast<int8_t *>(ctx->state + lp.off_h);
+    u.H = ctx->state + lp.off_h;
     u.W32 = reinterpret_cast<uint32_t *>(ctx->state + lp.off_w);
     u.Wq = ctx->state + lp.off_wq; u.ldq = lp.ldq_in;
     u.a32 = reinterpret_cast<const uint32_t *>(l == 1 ? d_x : reinterpret_cast<const uint64_t *>(
@@ -509,13 +509,21 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
   return BMLP_OK;
 }
 
-int bmlp_layer_views(bmlp_ctx *ctx, int32_t l, int8_t **d_h, uint64_t **d_w, uint64_t **d_p) {
+int bmlp_layer_views(bmlp_ctx *ctx, int32_t l, uint8_t **d_h, uint64_t **d_w, uint64_t **d_p) {
   if (ctx == nullptr) return BMLP_EINVAL;
   if (l < 1 || l > ctx->plan.L) return BMLP_ESHAPE;
   const LayerPlan &lp = ctx->plan.layer[l - 1];
-  if (d_h) *d_h = reinterpret_cast<int8_t *>(ctx->state + lp.off_h);
+  if (d_h) *d_h = ctx->state + lp.off_h;
   if (d_w) *d_w = reinterpret_cast<uint64_t *>(ctx->state + lp.off_w);
   if (d_p) *d_p = reinterpret_cast<uint64_t *>(ctx->state + lp.off_p);
+  return BMLP_OK;
+}
+
+int bmlp_read_h(bmlp_ctx *ctx, int32_t l, int8_t *d_out, void *stream) {
+  if (ctx == nullptr || d_out == nullptr) return BMLP_EINVAL;
+  if (l < 1 || l > ctx->plan.L) return BMLP_ESHAPE;
+  const LayerPlan &lp = ctx->plan.layer[l - 1];
+  BMLP_LAUNCH(launch_read_h(ctx->state + lp.off_h, lp.ld_h, lp.k_in, lp.k_out, d_out, as_stream(stream)));
   return BMLP_OK;
 }
 

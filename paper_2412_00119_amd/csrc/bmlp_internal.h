@@ -50,7 +50,8 @@ hipError_t launch_pack(const int8_t *x, int n, int K, uint64_t *bits, hipStream_
 
 // H_l and W_l of one layer from Philox stream 1 (init) or W_l from the H_l in
 // place (attach); P_l from stream 2.
-hipError_t launch_init_h(int8_t *H, int ld_h, uint64_t *W, int words_in, int k_in, int k_out,
+hipError_t launch_read_h(const uint8_t *H, int ld_h, int k_in, int k_out, int8_t *out, hipStream_t s);
+hipError_t launch_init_h(uint8_t *H, int ld_h, uint64_t *W, int words_in, int k_in, int k_out,
                          uint64_t seed, int layer, bool from_h, hipStream_t s);
 hipError_t launch_init_p(uint64_t *P, int words_out, int k_out, int c, uint64_t seed, int layer,
                          hipStream_t s);
@@ -133,7 +134,7 @@ hipError_t launch_eval_count(const int32_t *yhat, int c, const int32_t *y, int n
 // Clipped-Perceptron increments + reinforcement + clip + re-sign of up to
 // kMaxUpdLayers layers in one launch.
 struct UpdLayer {
-  int8_t *H;
+  uint8_t *H;              // bit-sliced [K_l][ld_h bytes]
   uint32_t *W32;
   uint8_t *Wq; int ldq;    // W_l as fp4 [K_l][ldq]
   const uint32_t *a32;     // a_{l-1} bit rows as 32-bit words [n][nw32]

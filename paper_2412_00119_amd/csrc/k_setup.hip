@@ -28,25 +28,57 @@ __device__ __forceinline__ bool stream_bit(uint64_t j, uint64_t seed, int layer,
 }
 
 // Grid: (ceil(ld_h / 256), k_out).  Thread = one column of one H row; each
-// wave covers 64 aligned columns and ballots the W word.
-__global__ __launch_bounds__(256) void init_h_kernel(int8_t *__restrict__ H, int ld_h,
+// wave covers 64 aligned columns, i.e. two 32-column groups of the bit-sliced
+// H (word p of a group = bit p of its 32 int8 values), and ballots both the
+// planes and the W word.  from_h: H is kept and only W = sign(H) is derived
+// (from the sign plane).
+__global__ __launch_bounds__(256) void init_h_kernel(uint8_t *__restrict__ H, int ld_h,
                                                      uint64_t *__restrict__ W, int words_in,
                                                      int k_in, int k_out, uint64_t seed, int layer,
                                                      int from_h) {
   const int k = blockIdx.y;
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (k >= k_out || i >= ld_h) return;    // ld_h is a multiple of 64: waves stay whole
-  int8_t h = 0;
+  const int lane = threadIdx.x & 63;
+  uint8_t *grp = H + (size_t)k * ld_h + (size_t)(i >> 5) * 32;   // this column's group
+  bool pos;
   if (from_h) {
-    h = i < k_in ? H[(size_t)k * ld_h + i] : (int8_t)0;
-  } else if (i < k_in) {
-    const uint64_t j = (uint64_t)k * (uint64_t)k_in + (uint64_t)i;
-    h = stream_bit(j, seed, layer, kStreamHInit) ? (int8_t)1 : (int8_t)-1;
+    const uint32_t sign = reinterpret_cast<const uint32_t *>(grp)[7];
+    pos = i < k_in && !((sign >> (i & 31)) & 1u);
+  } else {
+    int h = 0;   // padding columns hold 0
+    if (i < k_in) {
+      const uint64_t j = (uint64_t)k * (uint64_t)k_in + (uint64_t)i;
+      h = stream_bit(j, seed, layer, kStreamHInit) ? 1 : -1;
+    }
+    pos = h > 0;
+    uint32_t planes[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const uint64_t b = __ballot((h >> q) & 1);
+      planes[q] = (uint32_t)(b >> (lane & 32));
+    }
+    if ((lane & 31) == 0) {
+      reinterpret_cast<uint4 *>(grp)[0] = make_uint4(planes[0], planes[1], planes[2], planes[3]);
+      reinterpret_cast<uint4 *>(grp)[1] = make_uint4(planes[4], planes[5], planes[6], planes[7]);
+    }
   }
-  if (!from_h) H[(size_t)k * ld_h + i] = h;
-  const uint64_t m = __ballot(h > 0);
+  const uint64_t m = __ballot(pos);
   const int w = i >> 6;
-  if ((threadIdx.x & 63) == 0 && w < words_in) W[(size_t)k * words_in + w] = m;
+  if (lane == 0 && w < words_in) W[(size_t)k * words_in + w] = m;
+}
+
+// bit-sliced H [k_out][ld_h bytes] -> int8 [k_out][k_in]; one thread per value
+__global__ __launch_bounds__(256) void read_h_kernel(const uint8_t *__restrict__ H, int ld_h, int k_in,
+                                                     int k_out, int8_t *__restrict__ out) {
+  const int k = blockIdx.y;
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (k >= k_out || i >= k_in) return;
+  const uint32_t *grp = reinterpret_cast<const uint32_t *>(H + (size_t)k * ld_h + (size_t)(i >> 5) * 32);
+  uint32_t v = 0u;
+#pragma unroll
+  for (int q = 0; q < 8; ++q) v |= ((grp[q] >> (i & 31)) & 1u) << q;
+  out[(size_t)k * k_in + i] = (int8_t)(uint8_t)v;
 }
 
 // Grid: (ceil(words_out / 4), c).  One wave per 64 classifier entries.
@@ -89,10 +121,17 @@ hipError_t launch_pack(const int8_t *x, int n, int K, uint64_t *bits, hipStream_
   return hipGetLastError();
 }
 
-hipError_t launch_init_h(int8_t *H, int ld_h, uint64_t *W, int words_in, int k_in, int k_out,
+hipError_t launch_init_h(uint8_t *H, int ld_h, uint64_t *W, int words_in, int k_in, int k_out,
                          uint64_t seed, int layer, bool from_h, hipStream_t s) {
   hipLaunchKernelGGL(init_h_kernel, dim3(cdiv(ld_h, 256), k_out), dim3(256), 0, s, H, ld_h, W,
                      words_in, k_in, k_out, seed, layer, from_h ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_read_h(const uint8_t *H, int ld_h, int k_in, int k_out, int8_t *out, hipStream_t s) {
+  if (k_in <= 0 || k_out <= 0) return hipSuccess;
+  hipLaunchKernelGGL(read_h_kernel, dim3(cdiv(k_in, 256), k_out), dim3(256), 0, s, H, ld_h, k_in, k_out,
+                     out);
   return hipGetLastError();
 }
 

@@ -6,27 +6,35 @@
 //   dH[k][i] = 2 * sum over patterns mu that selected k of rho^{y^mu}_k a^mu_i,
 // then h <- clip(h + dH, -B, B); then every hidden weight whose 32-bit
 // Philox draw is below T_l moves one step away from zero, h <- clip(h +
-// 2 sign(h), -B, B); finally W = sign(H) is re-packed into bits.  A layer
-// whose M_l is empty is left untouched.
+// 2 sign(h), -B, B); finally W = sign(H) is written as bits and as fp4.  A
+// layer whose M_l is empty is left untouched.
+//
+// H is stored bit-sliced (see bmlp.h): each 32-column group of a row is eight
+// words, word p holding bit p of the 32 two's-complement int8 values.  A lane
+// owns one group, so every step below works on 32 columns with one bitwise
+// operation per bit plane:
+//   * the count cnt_i of +1 contributions (x = a-word XOR [rho = -1]) of the
+//     S selectors of the row is accumulated bit-sliced (plane p = bit p of
+//     the 32 counters), the loads of a-words issued eight at a time;
+//   * h + 4 cnt - 2 S (= h + dH) and the clip to [-B, B] are ripple-carry
+//     additions and comparisons on the planes, wide enough to be exact;
+//   * the coarse reinforcement bytes arrive as bit planes (one Philox word
+//     per plane), so "u8 < T >> 24" is an 8-step bit-sliced comparison; the
+//     fine 24 bits are drawn only where u8 == T >> 24;
+//   * h <- h + 2 sign(h) on the fired columns is one more planar addition,
+//     and W = sign(H) is the complement of the sign plane.
 //
 // Work item: (layer, group g, 2048-column chunk); a work-group of 8 waves.
 // The group's selections U_l (each pattern in M_l with a wrong perceptron in
-// the group) are bucketed by perceptron in LDS (counting sort),
-// then each wave walks whole rows with a lane owning 32 consecutive columns
-// (one 32-bit word of a_{l-1}).  With x = a-word XOR [rho = -1] the number
-// of +1 contributions per column is counted in bit-sliced form (plane p holds
-// bit p of the 32 counters), so one selector costs a short carry chain per
-// word; the counts are then spread into byte lanes and the clip is done on
-// packed 16-bit lanes: with cnt_i the count, sum_i = 2 cnt_i - S and
-// dH_i = 4 cnt_i - 2 S.  No two work-groups write the same bytes of H or W.
+// the group) are bucketed by perceptron in LDS (counting sort), then each
+// wave walks whole rows, lane l owning 32-column group chunk * 64 + l.  No two
+// work-groups write the same bytes of H or W.
 #include "bmlp_internal.h"
 #include "fp4.h"
 #include "philox.h"
 
 namespace bmlp {
 namespace {
-
-typedef short s16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
@@ -36,6 +44,10 @@ __device__ __forceinline__ int wave_sum(int v) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
   return v;
+}
+
+__device__ __forceinline__ uint32_t maj(uint32_t a, uint32_t b, uint32_t c) {
+  return (a & b) | (c & (a ^ b));
 }
 
 // bit-sliced increment of the 32 counters by the bits of x, planes [0, NP)
@@ -49,43 +61,113 @@ __device__ __forceinline__ void add_planes(uint32_t (&c)[kPlanes], uint32_t x) {
   }
 }
 
-struct SelCtx {
-  const uint16_t *list;
-  const uint32_t *a32;
-  int nw32, cw;
-  bool on;
-};
-
-// Adds selectors [s0, s1) of a row; after s selectors a counter is <= s, so
-// the carry chain of selector s (0-based) stops at plane floor(log2(s+1)).
 template <int NP>
-__device__ __forceinline__ void count_segment(uint32_t (&c)[kPlanes], const SelCtx &sc, int beg,
-                                              int s0, int s1) {
-  for (int s = s0; s < s1; ++s) {
-    const uint32_t ent = sc.list[beg + s];
-    const uint32_t mu = ent & 0x7FFFu;
-    const uint32_t flip = (ent & 0x8000u) ? 0xFFFFFFFFu : 0u;
-    const uint32_t x = (sc.on ? sc.a32[(size_t)mu * sc.nw32 + sc.cw] : 0u) ^ flip;
-    add_planes<NP>(c, x);
+__device__ __forceinline__ void add_batch(uint32_t (&c)[kPlanes], const uint32_t (&x)[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) add_planes<NP>(c, x[i]);
+}
+
+// Counts the +1 contributions of the row's S selectors (list[beg .. beg+S)),
+// eight selectors per batch so that their loads are in flight together.  A
+// batch past S loads a valid word (the row's last selector) and adds zero.
+__device__ __forceinline__ void count_row(uint32_t (&c)[kPlanes], const uint16_t *list, int beg, int S,
+                                          const uint32_t *a32, int nw32, int cw) {
+#pragma unroll
+  for (int q = 0; q < kPlanes; ++q) c[q] = 0u;
+  for (int s0 = 0; s0 < S; s0 += 8) {
+    uint32_t x[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int s = s0 + i;
+      const uint32_t ent = list[beg + min(s, S - 1)];
+      const uint32_t mu = ent & 0x7FFFu;
+      const uint32_t flip = (ent & 0x8000u) ? 0xFFFFFFFFu : 0u;
+      const uint32_t v = a32[(size_t)mu * nw32 + cw];
+      x[i] = s < S ? (v ^ flip) : 0u;
+    }
+    // planes in use after this batch: the counters are at most min(s0 + 8, S)
+    switch (32 - __clz(min(s0 + 8, S))) {
+      case 1: add_batch<1>(c, x); break;
+      case 2: add_batch<2>(c, x); break;
+      case 3: add_batch<3>(c, x); break;
+      case 4: add_batch<4>(c, x); break;
+      case 5: add_batch<5>(c, x); break;
+      case 6: add_batch<6>(c, x); break;
+      case 7: add_batch<7>(c, x); break;
+      case 8: add_batch<8>(c, x); break;
+      case 9: add_batch<9>(c, x); break;
+      case 10: add_batch<10>(c, x); break;
+      case 11: add_batch<11>(c, x); break;
+      case 12: add_batch<12>(c, x); break;
+      case 13: add_batch<13>(c, x); break;
+      case 14: add_batch<14>(c, x); break;
+      default: add_batch<15>(c, x); break;
+    }
   }
 }
 
-// Per-byte flags of (byte < t) for t in [0, 128], as bit 7 of each byte.
-__device__ __forceinline__ uint32_t bytes_lt(uint32_t x, uint32_t t) {
-  const uint32_t y = (x | 0x80808080u) - t * 0x01010101u;
-  return ~(y | x) & 0x80808080u;
+// x += k (mod 2^NB) for a constant k, bit-sliced.
+template <int NB>
+__device__ __forceinline__ void add_const(uint32_t (&x)[NB], uint32_t k) {
+  uint32_t carry = 0u;
+#pragma unroll
+  for (int p = 0; p < NB; ++p) {
+    const uint32_t kb = ((k >> p) & 1u) ? 0xFFFFFFFFu : 0u;
+    const uint32_t s = x[p] ^ kb ^ carry;
+    carry = maj(x[p], kb, carry);
+    x[p] = s;
+  }
 }
 
-// Gathers bit 7 of each byte into a 4-bit value (byte i -> bit i).
-__device__ __forceinline__ uint32_t gather_msb(uint32_t m) {
-  return (((m >> 7) * 0x01020408u) >> 24) & 0xFu;
+// Sign plane of x + k (mod 2^NB) for a constant k, bit-sliced (x unchanged).
+template <int NB>
+__device__ __forceinline__ uint32_t sign_of_sum(const uint32_t (&x)[NB], uint32_t k) {
+  uint32_t carry = 0u;
+#pragma unroll
+  for (int p = 0; p < NB - 1; ++p) {
+    const uint32_t kb = ((k >> p) & 1u) ? 0xFFFFFFFFu : 0u;
+    carry = maj(x[p], kb, carry);
+  }
+  const uint32_t kb = ((k >> (NB - 1)) & 1u) ? 0xFFFFFFFFu : 0u;
+  return x[NB - 1] ^ kb ^ carry;
 }
 
-// spread the 4 bits of n (n < 16) into bit 0 of the 4 bytes of a word
-__device__ __forceinline__ uint32_t spread4(uint32_t n) { return (n * 0x00204081u) & 0x01010101u; }
+// h <- clip(h + 4 cnt - 2 S, -B, B) on the 8 planes of h, computed in NB-bit
+// two's complement (exact: |h| <= 127 and 4 cnt <= 4 S).
+template <int NB>
+__device__ __forceinline__ void cp_apply(uint32_t (&h)[8], const uint32_t (&c)[kPlanes], int S, int B) {
+  // d = 4 cnt - 2 S
+  uint32_t z[NB];
+#pragma unroll
+  for (int p = 0; p < NB; ++p) z[p] = (p >= 2 && p - 2 < kPlanes) ? c[p - 2] : 0u;
+  add_const<NB>(z, (uint32_t)(-2 * S));
+  // z = h + d, h sign-extended
+  uint32_t carry = 0u;
+#pragma unroll
+  for (int p = 0; p < NB; ++p) {
+    const uint32_t hp = h[p < 8 ? p : 7];
+    const uint32_t s = z[p] ^ hp ^ carry;
+    carry = maj(z[p], hp, carry);
+    z[p] = s;
+  }
+  // z > B  <=>  z - (B + 1) >= 0 ;  z < -B  <=>  z + B < 0
+  const uint32_t gt = ~sign_of_sum<NB>(z, (uint32_t)(-(B + 1)));
+  const uint32_t lt = sign_of_sum<NB>(z, (uint32_t)B);
+#pragma unroll
+  for (int p = 0; p < 8; ++p) {
+    const uint32_t bp = ((B >> p) & 1) ? 0xFFFFFFFFu : 0u;     // plane p of +B
+    const uint32_t nbp = (((-B) >> p) & 1) ? 0xFFFFFFFFu : 0u;  // plane p of -B
+    h[p] = (z[p] & ~(gt | lt)) | (bp & gt) | (nbp & lt);
+  }
+}
 
-__device__ __forceinline__ s16x2 as_s16x2(uint32_t v) { return __builtin_bit_cast(s16x2, v); }
-__device__ __forceinline__ uint32_t as_u32(s16x2 v) { return __builtin_bit_cast(uint32_t, v); }
+// Lanes where the 8-plane value equals the constant v.
+__device__ __forceinline__ uint32_t equals(const uint32_t (&h)[8], int v) {
+  uint32_t e = 0xFFFFFFFFu;
+#pragma unroll
+  for (int p = 0; p < 8; ++p) e &= ((v >> p) & 1) ? h[p] : ~h[p];
+  return e;
+}
 
 __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   extern __shared__ int smem[];
@@ -162,17 +244,14 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   // bucket[r] is now the end of row r's selectors; row r starts at bucket[r-1]
 
   const int wave = tid >> 6, lane = tid & 63;
-  SelCtx sc;
-  sc.list = list;
-  sc.a32 = U.a32;
-  sc.nw32 = U.nw32;
-  sc.cw = chunk * 64 + lane;
-  sc.on = sc.cw < U.nw32;
-  const int cw = sc.cw;
+  const int cw = chunk * 64 + lane;        // this lane's 32-column group
+  const bool on = cw < U.nw32;
+  const int cwc = min(cw, U.nw32 - 1);     // clamped: loads stay inside the rows
   const int nvalid = min(max(U.k_in - cw * 32, 0), 32);
   const uint32_t validmask = nvalid == 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
   const int B = p.bound;
   const uint32_t t_hi = U.t_hi, t_lo = U.t_lo;
+  const int groups_in = (U.k_in + 31) >> 5;   // 32-column groups of a row holding columns
   int nreinf = 0;
 
   for (int r = wave; r < gamma; r += kWaves) {
@@ -180,125 +259,65 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     const int beg = r ? bucket[r - 1] : 0;
     const int S = bucket[r] - beg;
 
-    uint32_t hw[8];
-    int8_t *hrow = U.H + (size_t)k * U.ld_h + cw * 32;
-    if (sc.on) {
+    uint8_t *hrow = U.H + (size_t)k * U.ld_h + (size_t)cwc * 32;
+    uint32_t h[8];
+    {
       const uint4 h0 = reinterpret_cast<const uint4 *>(hrow)[0];
       const uint4 h1 = reinterpret_cast<const uint4 *>(hrow)[1];
-      hw[0] = h0.x; hw[1] = h0.y; hw[2] = h0.z; hw[3] = h0.w;
-      hw[4] = h1.x; hw[5] = h1.y; hw[6] = h1.z; hw[7] = h1.w;
+      h[0] = h0.x; h[1] = h0.y; h[2] = h0.z; h[3] = h0.w;
+      h[4] = h1.x; h[5] = h1.y; h[6] = h1.z; h[7] = h1.w;
     }
 
-    // ---- Clipped-Perceptron sum ---------------------------------------------
+    // ---- coarse reinforcement draws: plane p of the 32 bytes is word p of
+    // Philox blocks 2 (k ceil(K/32) + group) and the one after (stream 3) ----
+    const uint32_t blk = 2u * ((uint32_t)k * (uint32_t)groups_in + (uint32_t)cwc);
+    const U32x4 v0 = philox4x32_10(blk, U.ctr1, p.step, kStreamCoarse, p.key0, p.key1);
+    const U32x4 v1 = philox4x32_10(blk + 1u, U.ctr1, p.step, kStreamCoarse, p.key0, p.key1);
+
+    // ---- Clipped-Perceptron sum and clip ------------------------------------
     if (S > 0) {
       uint32_t c[kPlanes];
+      count_row(c, list, beg, S, U.a32, U.nw32, cwc);
+      uint32_t hn[8];
 #pragma unroll
-      for (int q = 0; q < kPlanes; ++q) c[q] = 0u;
-      count_segment<1>(c, sc, beg, 0, min(S, 1));
-      count_segment<2>(c, sc, beg, 1, min(S, 3));
-      count_segment<3>(c, sc, beg, 3, min(S, 7));
-      count_segment<4>(c, sc, beg, 7, min(S, 15));
-      count_segment<5>(c, sc, beg, 15, min(S, 31));
-      count_segment<6>(c, sc, beg, 31, min(S, 63));
-      count_segment<7>(c, sc, beg, 63, min(S, 127));
-      count_segment<8>(c, sc, beg, 127, min(S, 255));
-      if (S > 255) count_segment<kPlanes>(c, sc, beg, 255, S);
+      for (int q = 0; q < 8; ++q) hn[q] = h[q];
+      if (S <= 255)
+        cp_apply<11>(hn, c, S, B);
+      else
+        cp_apply<18>(hn, c, S, B);
+      // padding columns keep h = 0
+#pragma unroll
+      for (int q = 0; q < 8; ++q) h[q] = (hn[q] & validmask) | (h[q] & ~validmask);
+    }
 
-      if (sc.on) {
-        if (S <= 255) {
-          // counts as bytes, 4 columns per word
-          const int np = 32 - __clz(S);   // planes in use
-          const s16x2 lo2 = {(short)(128 - B), (short)(128 - B)};
-          const s16x2 hi2 = {(short)(128 + B), (short)(128 + B)};
-          const s16x2 m2 = {(short)(-2 * S), (short)(-2 * S)};
+    // ---- which weights reinforce: u8 < T >> 24, or u8 == T >> 24 and the
+    // fine 24 bits below T & 0xFFFFFF ---------------------------------------------
+    uint32_t fire, need;
+    if (t_hi >= 256u) {
+      fire = 0xFFFFFFFFu;
+      need = 0u;
+    } else {
+      const uint32_t rp[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+      uint32_t lt = 0u, eq = 0xFFFFFFFFu;
 #pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            uint32_t cb = 0u;
-#pragma unroll
-            for (int pl = 0; pl < 8; ++pl)
-              if (pl < np) cb |= spread4((c[pl] >> (4 * q)) & 0xFu) << pl;
-            // biased bytes hb = h + 128 in 16-bit lanes: columns (4q, 4q+1), (4q+2, 4q+3)
-            const uint32_t hb = hw[q] ^ 0x80808080u;
-            s16x2 h01 = as_s16x2((hb & 0xFFu) | ((hb & 0xFF00u) << 8));
-            s16x2 h23 = as_s16x2(((hb >> 16) & 0xFFu) | ((hb >> 8) & 0xFF0000u));
-            const s16x2 c01 = as_s16x2((cb & 0xFFu) | ((cb & 0xFF00u) << 8));
-            const s16x2 c23 = as_s16x2(((cb >> 16) & 0xFFu) | ((cb >> 8) & 0xFF0000u));
-            h01 = h01 + c01 * (s16x2){4, 4} + m2;
-            h23 = h23 + c23 * (s16x2){4, 4} + m2;
-            h01 = __builtin_elementwise_min(__builtin_elementwise_max(h01, lo2), hi2);
-            h23 = __builtin_elementwise_min(__builtin_elementwise_max(h23, lo2), hi2);
-            const uint32_t u01 = as_u32(h01), u23 = as_u32(h23);
-            const uint32_t nb = (u01 & 0xFFu) | ((u01 >> 8) & 0xFF00u) | ((u23 & 0xFFu) << 16) |
-                                ((u23 << 8) & 0xFF000000u);
-            // pad columns keep their bytes
-            const uint32_t vm = spread4((validmask >> (4 * q)) & 0xFu) * 0xFFu;
-            hw[q] = ((nb ^ 0x80808080u) & vm) | (hw[q] & ~vm);
-          }
+      for (int q = 7; q >= 0; --q) {
+        if ((t_hi >> q) & 1u) {
+          lt |= eq & ~rp[q];
+          eq &= rp[q];
         } else {
-          // more than 255 selectors: per-column integer counts
-#pragma unroll
-          for (int e = 0; e < 32; ++e) {
-            if (!((validmask >> e) & 1u)) continue;
-            int cnt = 0;
-#pragma unroll
-            for (int pl = 0; pl < kPlanes; ++pl) cnt |= (int)((c[pl] >> e) & 1u) << pl;
-            const int q = e >> 2, sh = 8 * (e & 3);
-            int h = (int)(int8_t)((hw[q] >> sh) & 0xFFu);
-            h = min(max(h + 4 * cnt - 2 * S, -B), B);
-            hw[q] = (hw[q] & ~(0xFFu << sh)) | (((uint32_t)h & 0xFFu) << sh);
-          }
+          eq &= ~rp[q];
         }
       }
-    }
-
-    if (!sc.on) continue;   // lanes past the row took part in the uniform loops only
-
-    // ---- reinforcement draws (Philox streams 3 and 4) -------------------------
-    const uint32_t j0 = (uint32_t)k * (uint32_t)U.k_in + (uint32_t)(cw * 32);
-    const uint32_t b0 = j0 >> 4, sh = j0 & 15u;
-    const U32x4 v0 = philox4x32_10(b0, U.ctr1, p.step, kStreamCoarse, p.key0, p.key1);
-    const U32x4 v1 = philox4x32_10(b0 + 1, U.ctr1, p.step, kStreamCoarse, p.key0, p.key1);
-    uint32_t u[8];
-    if (sh == 0) {
-      u[0] = v0.x; u[1] = v0.y; u[2] = v0.z; u[3] = v0.w;
-      u[4] = v1.x; u[5] = v1.y; u[6] = v1.z; u[7] = v1.w;
-    } else {
-      // weights j0.. start at byte sh of block b0: shift the 48 bytes of blocks
-      // b0..b0+2 down by sh bytes (sh is the same for the whole wave)
-      const U32x4 v2 = philox4x32_10(b0 + 2, U.ctr1, p.step, kStreamCoarse, p.key0, p.key1);
-      uint32_t w[12] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w, v2.x, v2.y, v2.z, v2.w};
-      if (sh & 4u) {
-#pragma unroll
-        for (int i = 0; i < 11; ++i) w[i] = w[i + 1];
-      }
-      if (sh & 8u) {
-#pragma unroll
-        for (int i = 0; i < 10; ++i) w[i] = w[i + 2];
-      }
-      const uint32_t bs = sh & 3u;
-#pragma unroll
-      for (int q = 0; q < 8; ++q)
-        u[q] = (uint32_t)((((uint64_t)w[q + 1] << 32) | w[q]) >> (8 * bs));
-    }
-    uint32_t fire = 0u, need = 0u;
-    if (t_hi <= 127) {
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const uint32_t lt = bytes_lt(u[q], t_hi);
-        const uint32_t le = bytes_lt(u[q], t_hi + 1);
-        fire |= gather_msb(lt) << (4 * q);
-        need |= gather_msb(le & ~lt) << (4 * q);
-      }
-    } else {
-#pragma unroll
-      for (int e = 0; e < 32; ++e) {
-        const uint32_t u8 = (u[e >> 2] >> (8 * (e & 3))) & 0xFFu;
-        fire |= (u8 < t_hi ? 1u : 0u) << e;
-        need |= (u8 == t_hi ? 1u : 0u) << e;
-      }
+      fire = lt;
+      need = eq;
     }
     fire &= validmask;
     need &= validmask;
+    if (!on) {
+      fire = 0u;
+      need = 0u;
+    }
+    const uint32_t j0 = (uint32_t)k * (uint32_t)U.k_in + (uint32_t)(cwc * 32);
     while (need) {
       const int e = __ffs(need) - 1;
       need &= need - 1u;
@@ -308,27 +327,27 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     }
     nreinf += __popc(fire);
 
-    // ---- h <- clip(h + 2 sign(h)) on the (rare) fired weights ---------------------
+    // ---- h <- clip(h + 2 sign(h)) on the fired weights: |h| = B stays ----------
+    {
+      const uint32_t gmask = fire & ~(equals(h, B) | equals(h, -B));
+      const uint32_t neg = gmask & h[7];
+      // add delta = +2 (0000 0010) or -2 (1111 1110) where gmask is set
+      uint32_t carry = h[1] & gmask;
+      h[1] ^= gmask;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      uint32_t m = (fire >> (4 * q)) & 0xFu;
-      while (m) {
-        const int b = __ffs(m) - 1;
-        m &= m - 1u;
-        const int shb = 8 * b;
-        int h = (int)(int8_t)((hw[q] >> shb) & 0xFFu);
-        h = min(max(h + (h > 0 ? 2 : -2), -B), B);
-        hw[q] = (hw[q] & ~(0xFFu << shb)) | (((uint32_t)h & 0xFFu) << shb);
+      for (int q = 2; q < 8; ++q) {
+        const uint32_t s = h[q] ^ neg ^ carry;
+        carry = maj(h[q], neg, carry);
+        h[q] = s;
       }
     }
 
-    // ---- store H and W = sign(H) (h is odd: positive iff the sign bit is clear) ----
-    uint32_t wbits = 0u;
-#pragma unroll
-    for (int q = 0; q < 8; ++q) wbits |= gather_msb(~hw[q] & 0x80808080u) << (4 * q);
-    wbits &= validmask;
-    reinterpret_cast<uint4 *>(hrow)[0] = make_uint4(hw[0], hw[1], hw[2], hw[3]);
-    reinterpret_cast<uint4 *>(hrow)[1] = make_uint4(hw[4], hw[5], hw[6], hw[7]);
+    if (!on) continue;   // lanes past the row took part in the uniform loops only
+
+    // ---- store H and W = sign(H) (h is odd, so the sign plane decides) -------
+    const uint32_t wbits = ~h[7] & validmask;
+    reinterpret_cast<uint4 *>(hrow)[0] = make_uint4(h[0], h[1], h[2], h[3]);
+    reinterpret_cast<uint4 *>(hrow)[1] = make_uint4(h[4], h[5], h[6], h[7]);
     U.W32[(size_t)k * U.nw32 + cw] = wbits;
     {
       uint32_t o[4];

@@ -72,9 +72,9 @@ def test_stress_workload_sampled():
         nreinf = 0
         if upd.any():
             j = (rows[:, None].astype(np.uint64) * np.uint64(kin) + np.arange(kin, dtype=np.uint64)).ravel()
-            mask = ob.reinforce_draws(cfg.seed, l, t, j) < np.uint64(T)
+            mask = ob.reinforce_draws(cfg.seed, l, t, j, kin) < np.uint64(T)
             h = ob.reinforce(h, mask, cfg.bound)
-            nreinf = int(ob.reinforce_mask(cfg.seed, l, t, T, kin * kout).sum())
+            nreinf = int(ob.reinforce_mask(cfg.seed, l, t, T, kin * kout, kin).sum())
         want_stats = np.array([err.sum(), upd.sum(), (kstar >= 0).sum(), nreinf], dtype=np.int64)
         np.testing.assert_array_equal(st[l - 1], want_stats, err_msg=f"stats_{l}")
         Hg = net.H(l)[torch.from_numpy(rows).cuda()].cpu().numpy()

@@ -91,14 +91,23 @@ def test_prefix_bits_match_gathered_bits(n):
                                       ob.stream_bits(0x1234_5678_9ABC, 2, stream, np.arange(n, dtype=np.uint64)))
 
 
-def test_reinforce_draws_layout():
-    j = np.arange(64, dtype=np.uint64)
-    u = ob.reinforce_draws(7, 2, 5, j)
-    cw = np.stack(philox4x32_10(np.arange(4, dtype=np.uint64), 1, 5, ob.STREAM_R_COARSE, 7, 0), axis=-1)
-    fw = np.stack(philox4x32_10(np.arange(16, dtype=np.uint64), 1, 5, ob.STREAM_R_FINE, 7, 0), axis=-1)
-    u8 = cw.astype("<u4").view(np.uint8).reshape(-1)
-    u24 = fw.reshape(-1) & 0xFFFFFF
-    np.testing.assert_array_equal(u, (u8.astype(np.uint64) << 24) | u24.astype(np.uint64))
+@pytest.mark.parametrize("k_in", [40, 64, 100])
+def test_reinforce_draws_layout(k_in):
+    """u8 of weight (k, i): bit p is bit (i & 31) of word p of the two stream-3
+    blocks of the row's 32-column group; u24 comes from stream 4 by flat index."""
+    j = np.arange(3 * k_in, dtype=np.uint64)
+    u = ob.reinforce_draws(7, 2, 5, j, k_in)
+    groups = (k_in + 31) // 32
+    expect = []
+    for jj in range(3 * k_in):
+        k, i = divmod(jj, k_in)
+        q = k * groups + (i >> 5)
+        planes = [int(w) for w in philox4x32_10(2 * q, 1, 5, ob.STREAM_R_COARSE, 7, 0)]
+        planes += [int(w) for w in philox4x32_10(2 * q + 1, 1, 5, ob.STREAM_R_COARSE, 7, 0)]
+        u8 = sum(((planes[p] >> (i & 31)) & 1) << p for p in range(8))
+        u24 = int(philox4x32_10(jj >> 2, 1, 5, ob.STREAM_R_FINE, 7, 0)[jj & 3]) & 0xFFFFFF
+        expect.append((u8 << 24) | u24)
+    np.testing.assert_array_equal(u, np.array(expect, dtype=np.uint64))
 
 
 def test_reinforcement_rate_binomial():
@@ -107,14 +116,14 @@ def test_reinforcement_rate_binomial():
     for p_r, k in [(0.5, 4096), (0.5, 256), (0.05, 1024), (2.0, 64)]:
         T = ob.reinforce_threshold(p_r, k)
         q = T / 2**32
-        m = ob.reinforce_mask(1234, 1, 17, T, n)
+        m = ob.reinforce_mask(1234, 1, 17, T, n, 4096)
         sd = math.sqrt(n * q * (1 - q))
         assert abs(m.sum() - n * q) < 5 * sd + 1, (p_r, k, m.sum(), n * q)
 
 
 def test_draws_are_uniform_bytes():
     """Chi-square of the top byte of the 32-bit draws over 2^20 samples."""
-    u = ob.reinforce_draws(99, 1, 3, np.arange(1 << 20, dtype=np.uint64))
+    u = ob.reinforce_draws(99, 1, 3, np.arange(1 << 20, dtype=np.uint64), 1000)
     top = (u >> np.uint64(24)).astype(np.int64)
     hist = np.bincount(top, minlength=256)
     e = len(top) / 256
@@ -128,10 +137,10 @@ def test_draws_are_uniform_bytes():
 
 def test_streams_and_steps_differ():
     j = np.arange(4096, dtype=np.uint64)
-    a = ob.reinforce_draws(1, 1, 0, j)
-    b = ob.reinforce_draws(1, 1, 1, j)
-    c = ob.reinforce_draws(1, 2, 0, j)
-    d = ob.reinforce_draws(2, 1, 0, j)
+    a = ob.reinforce_draws(1, 1, 0, j, 512)
+    b = ob.reinforce_draws(1, 1, 1, j, 512)
+    c = ob.reinforce_draws(1, 2, 0, j, 512)
+    d = ob.reinforce_draws(2, 1, 0, j, 512)
     for other in (b, c, d):
         assert (a == other).mean() < 0.01
 
