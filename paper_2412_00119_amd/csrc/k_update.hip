@@ -15,7 +15,8 @@
 // operation per bit plane:
 //   * the count cnt_i of +1 contributions (x = a-word XOR [rho = -1]) of the
 //     S selectors of the row is accumulated bit-sliced (plane p = bit p of
-//     the 32 counters), the loads of a-words issued eight at a time;
+//     the 32 counters) with carry-save adder trees, the loads of a row's
+//     a-words issued sixteen at a time;
 //   * h + 4 cnt - 2 S (= h + dH) and the clip to [-B, B] are ripple-carry
 //     additions and comparisons on the planes, wide enough to be exact;
 //   * the coarse reinforcement bytes arrive as bit planes (one Philox word
@@ -24,11 +25,11 @@
 //   * h <- h + 2 sign(h) on the fired columns is one more planar addition,
 //     and W = sign(H) is the complement of the sign plane.
 //
-// Work item: (layer, group g, 2048-column chunk); a work-group of 8 waves.
-// The group's selections U_l (each pattern in M_l with a wrong perceptron in
-// the group) are bucketed by perceptron in LDS (counting sort), then each
-// wave walks whole rows, lane l owning 32-column group chunk * 64 + l.  No two
-// work-groups write the same bytes of H or W.
+// Work-group: (layer, group g), 16 waves.  The group's selections U_l (each
+// pattern in M_l with a wrong perceptron in the group) are bucketed by
+// perceptron in LDS (counting sort), then the waves take the group's (row,
+// 2048-column chunk) items, lane l owning 32-column group chunk * 64 + l.  No
+// two work-groups write the same bytes of H or W.
 #include "bmlp_internal.h"
 #include "fp4.h"
 #include "philox.h"
@@ -36,7 +37,7 @@
 namespace bmlp {
 namespace {
 
-constexpr int kWaves = 8;
+constexpr int kWaves = 16;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kPlanes = 15;   // counts up to 2^15 - 1 >= BMLP_MAX_BATCH
 
@@ -50,58 +51,134 @@ __device__ __forceinline__ uint32_t maj(uint32_t a, uint32_t b, uint32_t c) {
   return (a & b) | (c & (a ^ b));
 }
 
-// bit-sliced increment of the 32 counters by the bits of x, planes [0, NP)
-template <int NP>
-__device__ __forceinline__ void add_planes(uint32_t (&c)[kPlanes], uint32_t x) {
+// Carry-save compression: a full adder turns three bit-vectors of one
+// weight into a sum of that weight and a carry of twice it (two 3-input
+// bitwise operations), a half adder does the same for two.
+__device__ __forceinline__ void fa(uint32_t a, uint32_t b, uint32_t c, uint32_t &s, uint32_t &cy) {
+  s = a ^ b ^ c;
+  cy = maj(a, b, c);
+}
+__device__ __forceinline__ void ha(uint32_t a, uint32_t b, uint32_t &s, uint32_t &cy) {
+  s = a ^ b;
+  cy = a & b;
+}
+
+// Per lane, the number of set bits among x[0..8) as 4 planes n[0..4).
+__device__ __forceinline__ void compress8(const uint32_t (&x)[8], uint32_t (&n)[4]) {
+  uint32_t a, b, c, d, e, f, s1, c1, s2, c2, t, u;
+  fa(x[0], x[1], x[2], a, b);    // a:1 b:2
+  fa(x[3], x[4], x[5], c, d);    // c:1 d:2
+  fa(x[6], x[7], a, e, f);       // e:1 f:2
+  ha(c, e, n[0], s1);            // n0:1 s1:2
+  fa(b, d, f, s2, c1);           // s2:2 c1:4
+  ha(s2, s1, n[1], c2);          // n1:2 c2:4
+  ha(c1, c2, t, u);              // t:4 u:8
+  n[2] = t;
+  n[3] = u;
+}
+
+// Per lane, the number of set bits among x[0..16) as 5 planes n[0..5).
+__device__ __forceinline__ void compress16(const uint32_t (&x)[16], uint32_t (&n)[5]) {
+  // weight 1: 16 bits
+  uint32_t s[6], c2[8];
+  fa(x[0], x[1], x[2], s[0], c2[0]);
+  fa(x[3], x[4], x[5], s[1], c2[1]);
+  fa(x[6], x[7], x[8], s[2], c2[2]);
+  fa(x[9], x[10], x[11], s[3], c2[3]);
+  fa(x[12], x[13], x[14], s[4], c2[4]);
+  uint32_t t0, t1;
+  fa(s[0], s[1], s[2], t0, c2[5]);
+  fa(s[3], s[4], x[15], t1, c2[6]);
+  ha(t0, t1, n[0], c2[7]);
+  // weight 2: 8 bits
+  uint32_t w2a, w2b, w2c, c4[4];
+  fa(c2[0], c2[1], c2[2], w2a, c4[0]);
+  fa(c2[3], c2[4], c2[5], w2b, c4[1]);
+  fa(c2[6], c2[7], w2a, w2c, c4[2]);
+  ha(w2b, w2c, n[1], c4[3]);
+  // weight 4: 4 bits
+  uint32_t w4a, c8a, c8b;
+  fa(c4[0], c4[1], c4[2], w4a, c8a);
+  ha(w4a, c4[3], n[2], c8b);
+  // weight 8: 2 bits
+  ha(c8a, c8b, n[3], n[4]);
+}
+
+// c += n (n has NN planes), rippling the carry up to plane NP - 1.
+template <int NN, int NP>
+__device__ __forceinline__ void add_count(uint32_t (&c)[kPlanes], const uint32_t (&n)[NN]) {
+  uint32_t carry = 0u;
 #pragma unroll
   for (int p = 0; p < NP; ++p) {
-    const uint32_t t = c[p] & x;
-    c[p] ^= x;
-    x = t;
+    if (p < NN) {
+      const uint32_t sum = c[p] ^ n[p] ^ carry;
+      carry = maj(c[p], n[p], carry);
+      c[p] = sum;
+    } else {
+      const uint32_t sum = c[p] ^ carry;
+      carry = c[p] & carry;
+      c[p] = sum;
+    }
   }
 }
 
-template <int NP>
-__device__ __forceinline__ void add_batch(uint32_t (&c)[kPlanes], const uint32_t (&x)[8]) {
+// Loads the a-words of selectors s0 .. s0 + N - 1 of a row (list[beg + s]),
+// flipped where rho = -1, all loads in flight together; entries past S load a
+// valid word (the row's last selector) and become zero.
+template <int N>
+__device__ __forceinline__ void load_selectors(uint32_t (&x)[N], const uint16_t *list, int beg, int S, int s0,
+                                               const uint32_t *a32, int nw32, int cw) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) add_planes<NP>(c, x[i]);
+  for (int i = 0; i < N; ++i) {
+    const int s = s0 + i;
+    // every lane reads the same entry: make it a scalar
+    const uint32_t ent = __builtin_amdgcn_readfirstlane(list[beg + min(s, S - 1)]);
+    const uint32_t mu = ent & 0x7FFFu;
+    const uint32_t flip = (s < S) ? ((ent & 0x8000u) ? 0xFFFFFFFFu : 0u) : 0u;
+    const uint32_t keep = (s < S) ? 0xFFFFFFFFu : 0u;
+    x[i] = (a32[(size_t)mu * nw32 + cw] ^ flip) & keep;
+  }
 }
 
-// Counts the +1 contributions of the row's S selectors (list[beg .. beg+S)),
-// eight selectors per batch so that their loads are in flight together.  A
-// batch past S loads a valid word (the row's last selector) and adds zero.
+// Counts the +1 contributions of the row's S >= 1 selectors (list[beg ..
+// beg+S)) into bit-sliced counters: up to 8, or else the first 16, through a
+// carry-save tree, the rest 8 at a time added to the running count.
 __device__ __forceinline__ void count_row(uint32_t (&c)[kPlanes], const uint16_t *list, int beg, int S,
                                           const uint32_t *a32, int nw32, int cw) {
 #pragma unroll
   for (int q = 0; q < kPlanes; ++q) c[q] = 0u;
-  for (int s0 = 0; s0 < S; s0 += 8) {
-    uint32_t x[8];
+  if (S <= 8) {
+    uint32_t x[8], n[4];
+    load_selectors<8>(x, list, beg, S, 0, a32, nw32, cw);
+    compress8(x, n);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int s = s0 + i;
-      const uint32_t ent = list[beg + min(s, S - 1)];
-      const uint32_t mu = ent & 0x7FFFu;
-      const uint32_t flip = (ent & 0x8000u) ? 0xFFFFFFFFu : 0u;
-      const uint32_t v = a32[(size_t)mu * nw32 + cw];
-      x[i] = s < S ? (v ^ flip) : 0u;
-    }
+    for (int q = 0; q < 4; ++q) c[q] = n[q];
+    return;
+  }
+  {
+    uint32_t x[16], n[5];
+    load_selectors<16>(x, list, beg, S, 0, a32, nw32, cw);
+    compress16(x, n);
+#pragma unroll
+    for (int q = 0; q < 5; ++q) c[q] = n[q];
+  }
+  for (int s0 = 16; s0 < S; s0 += 8) {
+    uint32_t x[8], n[4];
+    load_selectors<8>(x, list, beg, S, s0, a32, nw32, cw);
+    compress8(x, n);
     // planes in use after this batch: the counters are at most min(s0 + 8, S)
     switch (32 - __clz(min(s0 + 8, S))) {
-      case 1: add_batch<1>(c, x); break;
-      case 2: add_batch<2>(c, x); break;
-      case 3: add_batch<3>(c, x); break;
-      case 4: add_batch<4>(c, x); break;
-      case 5: add_batch<5>(c, x); break;
-      case 6: add_batch<6>(c, x); break;
-      case 7: add_batch<7>(c, x); break;
-      case 8: add_batch<8>(c, x); break;
-      case 9: add_batch<9>(c, x); break;
-      case 10: add_batch<10>(c, x); break;
-      case 11: add_batch<11>(c, x); break;
-      case 12: add_batch<12>(c, x); break;
-      case 13: add_batch<13>(c, x); break;
-      case 14: add_batch<14>(c, x); break;
-      default: add_batch<15>(c, x); break;
+      case 5: add_count<4, 5>(c, n); break;
+      case 6: add_count<4, 6>(c, n); break;
+      case 7: add_count<4, 7>(c, n); break;
+      case 8: add_count<4, 8>(c, n); break;
+      case 9: add_count<4, 9>(c, n); break;
+      case 10: add_count<4, 10>(c, n); break;
+      case 11: add_count<4, 11>(c, n); break;
+      case 12: add_count<4, 12>(c, n); break;
+      case 13: add_count<4, 13>(c, n); break;
+      case 14: add_count<4, 14>(c, n); break;
+      default: add_count<4, 15>(c, n); break;
     }
   }
 }
@@ -133,7 +210,9 @@ __device__ __forceinline__ uint32_t sign_of_sum(const uint32_t (&x)[NB], uint32_
 }
 
 // h <- clip(h + 4 cnt - 2 S, -B, B) on the 8 planes of h, computed in NB-bit
-// two's complement (exact: |h| <= 127 and 4 cnt <= 4 S).
+// two's complement.  NB must hold 4 S, and z - (B + 1) and z + B for
+// z = h + 4 cnt - 2 S: 10 bits for S <= 63, 11 for S <= 255, 18 for S <=
+// 16383 (|h|, B <= 127).
 template <int NB>
 __device__ __forceinline__ void cp_apply(uint32_t (&h)[8], const uint32_t (&c)[kPlanes], int S, int B) {
   // d = 4 cnt - 2 S
@@ -171,26 +250,25 @@ __device__ __forceinline__ uint32_t equals(const uint32_t (&h)[8], int v) {
 
 __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   extern __shared__ int smem[];
-  __shared__ int part[kThreads];
+  __shared__ int wsum[kWaves];
+  __shared__ int s_sel;
 
   const int tid = threadIdx.x;
-  // ---- which layer / group / chunk ------------------------------------------
+  const int wave = tid >> 6, lane = tid & 63;
+  // ---- which layer / group ---------------------------------------------------
   int li = 0;
 #pragma unroll 1
   for (int i = 1; i < p.nl; ++i)
     if ((int)blockIdx.x >= p.L[i].block0) li = i;
   const UpdLayer &U = p.L[li];
   if (U.stats[1] == 0) return;   // M_l empty: Algorithm 2 is not run for this layer
-  const int rel = (int)blockIdx.x - U.block0;
-  const int g = rel / U.chunks;
-  const int chunk = rel % U.chunks;
+  const int g = (int)blockIdx.x - U.block0;
   const int gamma = U.gamma;
   int *bucket = smem;                                            // [gamma]
   uint16_t *list = reinterpret_cast<uint16_t *>(smem + gamma);   // [n]
   const int16_t *kcol = U.kstar + (size_t)g * p.ldk;
 
   // ---- bucket the selections of group g by perceptron (counting sort) -------
-  __shared__ int s_sel;
   if (tid == 0) s_sel = 0;
   for (int r = tid; r < gamma; r += kThreads) bucket[r] = 0;
   __syncthreads();
@@ -203,26 +281,27 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
       ++nsel;
     }
   }
-  if (chunk == 0) {   // |U_l|, counted once per group
-    nsel = wave_sum(nsel);
-    if ((tid & 63) == 0 && nsel) atomicAdd(&s_sel, nsel);
-  }
+  nsel = wave_sum(nsel);
+  if (lane == 0 && nsel) atomicAdd(&s_sel, nsel);
   __syncthreads();
-  if (chunk == 0 && tid == 0 && s_sel) atomicAdd(U.stats + 2, s_sel);
+  if (tid == 0 && s_sel) atomicAdd(U.stats + 2, s_sel);   // |U_l|
   {
+    // exclusive prefix sum of the bucket sizes: thread t owns buckets
+    // [t ch, t ch + ch); a scan inside each wave, then across the waves
     const int ch = (gamma + kThreads - 1) / kThreads;
     const int b0 = min(gamma, tid * ch), b1 = min(gamma, b0 + ch);
-    int s = 0;
-    for (int r = b0; r < b1; ++r) s += bucket[r];
-    part[tid] = s;
-    __syncthreads();
-    for (int o = 1; o < kThreads; o <<= 1) {
-      const int v = tid >= o ? part[tid - o] : 0;
-      __syncthreads();
-      part[tid] += v;
-      __syncthreads();
+    int own = 0;
+    for (int r = b0; r < b1; ++r) own += bucket[r];
+    int inc = own;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int v = __shfl_up(inc, d, 64);
+      if (lane >= d) inc += v;
     }
-    int run = part[tid] - s;
+    if (lane == 63) wsum[wave] = inc;
+    __syncthreads();
+    int run = inc - own;
+    for (int w = 0; w < wave; ++w) run += wsum[w];
     for (int r = b0; r < b1; ++r) {
       const int c = bucket[r];
       bucket[r] = run;
@@ -243,21 +322,26 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   __syncthreads();
   // bucket[r] is now the end of row r's selectors; row r starts at bucket[r-1]
 
-  const int wave = tid >> 6, lane = tid & 63;
-  const int cw = chunk * 64 + lane;        // this lane's 32-column group
-  const bool on = cw < U.nw32;
-  const int cwc = min(cw, U.nw32 - 1);     // clamped: loads stay inside the rows
-  const int nvalid = min(max(U.k_in - cw * 32, 0), 32);
-  const uint32_t validmask = nvalid == 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
   const int B = p.bound;
   const uint32_t t_hi = U.t_hi, t_lo = U.t_lo;
   const int groups_in = (U.k_in + 31) >> 5;   // 32-column groups of a row holding columns
   int nreinf = 0;
 
-  for (int r = wave; r < gamma; r += kWaves) {
+  // work items: (row r, 2048-column chunk); lane l owns 32-column group
+  // chunk * 64 + l of the row
+  const int items = gamma * U.chunks;
+  for (int it = wave; it < items; it += kWaves) {
+    const int r = it / U.chunks, chunk = it - r * U.chunks;
     const int k = g * gamma + r;
-    const int beg = r ? bucket[r - 1] : 0;
-    const int S = bucket[r] - beg;
+    const int cw = chunk * 64 + lane;
+    const bool on = cw < U.nw32;
+    const int cwc = min(cw, U.nw32 - 1);     // clamped: loads stay inside the rows
+    const int nvalid = min(max(U.k_in - cw * 32, 0), 32);
+    const uint32_t validmask = nvalid == 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
+    // the row's selector range is the same for every lane: scalars, so the
+    // branches on S are scalar and its constants live in scalar registers
+    const int beg = __builtin_amdgcn_readfirstlane(r ? bucket[r - 1] : 0);
+    const int S = __builtin_amdgcn_readfirstlane(bucket[r]) - beg;
 
     uint8_t *hrow = U.H + (size_t)k * U.ld_h + (size_t)cwc * 32;
     uint32_t h[8];
@@ -281,7 +365,9 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
       uint32_t hn[8];
 #pragma unroll
       for (int q = 0; q < 8; ++q) hn[q] = h[q];
-      if (S <= 255)
+      if (S <= 63)
+        cp_apply<10>(hn, c, S, B);
+      else if (S <= 255)
         cp_apply<11>(hn, c, S, B);
       else
         cp_apply<18>(hn, c, S, B);
@@ -336,13 +422,13 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
       h[1] ^= gmask;
 #pragma unroll
       for (int q = 2; q < 8; ++q) {
-        const uint32_t s = h[q] ^ neg ^ carry;
+        const uint32_t sum = h[q] ^ neg ^ carry;
         carry = maj(h[q], neg, carry);
-        h[q] = s;
+        h[q] = sum;
       }
     }
 
-    if (!on) continue;   // lanes past the row took part in the uniform loops only
+    if (!on) continue;   // lanes past the row took part in the uniform steps only
 
     // ---- store H and W = sign(H) (h is odd, so the sign plane decides) -------
     const uint32_t wbits = ~h[7] & validmask;
@@ -358,11 +444,12 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   }
 
   nreinf = wave_sum(nreinf);
-  if (lane == 0) part[wave] = nreinf;
+  __syncthreads();   // wsum is free again
+  if (lane == 0) wsum[wave] = nreinf;
   __syncthreads();
   if (tid == 0) {
     int t = 0;
-    for (int w = 0; w < kWaves; ++w) t += part[w];
+    for (int w = 0; w < kWaves; ++w) t += wsum[w];
     if (t) atomicAdd(U.stats + 3, t);   // one atomic per work-group
   }
 }
@@ -381,7 +468,7 @@ hipError_t launch_update(UpdateBatch &b, hipStream_t s) {
     UpdLayer &u = b.L[i];
     u.chunks = (u.nw32 + 63) / 64;
     u.block0 = blocks;
-    blocks += u.groups * u.chunks;
+    blocks += u.groups;
     gmax = max(gmax, u.gamma);
   }
   hipLaunchKernelGGL(update_kernel, dim3(blocks), dim3(kThreads), update_lds_bytes(gmax, b.n), s, b);
