@@ -172,7 +172,7 @@ def main():
     log(f"workload {w.name}: widths {w.widths} c={w.n_classes} B={w.bound} bs={w.batch}")
     xs, ys = make_batches(w, torch, net, max_batches=48)
     nb = len(xs)
-    stats = torch.empty((w.n_layers, 4), dtype=torch.int32, device="cuda")
+    stats = torch.empty((w.n_layers, B.STATS_STRIDE), dtype=torch.int32, device="cuda")
     t = 0
 
     def run(k):

@@ -196,9 +196,13 @@ int bmlp_forward(bmlp_ctx *ctx, const uint64_t *d_x, int32_t n, int32_t *d_yhat,
  *            restored from a checkpoint continues bit-exactly.
  *   p_r      reinforcement probability of this step (the epoch rescale
  *            p_r <- p_r sqrt(E^e) stays with the caller).
- *   d_stats  int32 [L][4], overwritten with per-layer counts: sum of the
+ *   d_stats  int32 [L][BMLP_STATS_STRIDE], 8-byte aligned; entries 0..3 of
+ *            row l-1 are overwritten with layer l's counts: sum of the
  *            01-loss, |M_l|, |U_l| (selected pairs), and reinforcement draws
  *            that fired (0 when M_l is empty, as the layer is then untouched).
+ *            The other entries of a row are scratch.  Each layer's counts
+ *            sit in a 128-byte line of their own, so the work-groups adding
+ *            to them do not queue on one cache line.
  * Every layer's forward uses the weights from before the step. */
 int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int32_t n,
                     uint64_t step, double p_r, int32_t *d_stats, void *stream);
@@ -229,6 +233,9 @@ const char *bmlp_status_string(int status);
 
 /* Message of the last BMLP_EHIP on this thread ("" if none). */
 const char *bmlp_last_error(void);
+
+/* int32 entries per layer row of bmlp_train_step's d_stats (128 bytes). */
+#define BMLP_STATS_STRIDE 32
 
 /* Kernel classes timed by the profiling aid below. */
 enum {

@@ -192,6 +192,7 @@ def bmlp_destroy(ctx: int):
     lib().bmlp_destroy(ctx)
 
 
+STATS_STRIDE = 32   # BMLP_STATS_STRIDE: int32 entries per layer row of the step statistics
 KERNEL_KINDS = ("fwd", "cls", "select", "update", "other")
 
 
@@ -283,13 +284,19 @@ class BMLP:
 
     # ---- the method -----------------------------------------------------------
     def train_step(self, x_bits, y, step: int, p_r: float, stats=None):
-        """One mini-batch; returns int32 stats [L][4] (err, |M|, |U|, reinforced)."""
+        """One mini-batch; returns int32 stats [L][4] (err, |M|, |U|, reinforced).
+
+        ``stats``, if given, is an int32 tensor [L][BMLP_STATS_STRIDE] that the
+        library fills (each layer's counts in a 128-byte row of their own)."""
         n = self._batch(x_bits, y)
         if stats is None:
-            stats = self.torch.empty((self.n_layers, 4), dtype=self.torch.int32, device=self.device)
+            stats = self.torch.empty((self.n_layers, STATS_STRIDE), dtype=self.torch.int32, device=self.device)
+        if tuple(stats.shape) != (self.n_layers, STATS_STRIDE) or stats.dtype != self.torch.int32 \
+                or not stats.is_contiguous():
+            raise ValueError(f"stats must be a contiguous int32 tensor [{self.n_layers}][{STATS_STRIDE}]")
         bmlp_train_step(self.ctx, x_bits.data_ptr(), y.data_ptr(), n, int(step), float(p_r),
                         stats.data_ptr(), self._stream())
-        return stats
+        return stats[:, :4]
 
     def forward(self, x_bits):
         """Local outputs y_hat of every layer, int32 [L][n][c]."""

@@ -398,20 +398,22 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
   int st = check_ctx_batch(ctx, d_x, n);
   if (st != BMLP_OK) return st;
   if (d_stats == nullptr || (n > 0 && d_y == nullptr)) return BMLP_EINVAL;
+  if (reinterpret_cast<uintptr_t>(d_stats) & 7) return BMLP_EINVAL;
   if (!(p_r >= 0.0) || !isfinite(p_r)) return BMLP_EINVAL;
   const Plan &p = ctx->plan;
   hipStream_t s = as_stream(stream);
   const bool mfma = use_mfma(p);
   ProfScope prof_scope{ctx};
   if (n == 0 || !mfma)
-    BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s, launch_fill_i32(d_stats, 4 * p.L, 0, s));
+    BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s, launch_fill_i32(d_stats, BMLP_STATS_STRIDE * p.L, 0, s));
   if (n == 0) return BMLP_OK;
   int16_t *z = reinterpret_cast<int16_t *>(ctx->ws + p.off_z);
   int32_t *yh = reinterpret_cast<int32_t *>(ctx->ws + p.off_yhat);
   uint8_t *xq = ctx->ws + p.off_xq;
   if (mfma)   // input as fp4 rows; also zeroes the statistics
     BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s,
-               launch_fp4_rows(d_x, p.layer[0].words_in, p.widths[0], n, xq, p.ldq0, d_stats, 4 * p.L, s));
+               launch_fp4_rows(d_x, p.layer[0].words_in, p.widths[0], n, xq, p.ldq0, d_stats,
+                               BMLP_STATS_STRIDE * p.L, s));
   const uint64_t *a_prev = d_x;
   const uint8_t *aq_prev = xq;
   for (int l = 1; l <= p.L; ++l) {
@@ -422,7 +424,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
     uint8_t *err = ctx->ws + lp.off_err;
     uint8_t *upd = ctx->ws + lp.off_upd;
     int16_t *kstar = reinterpret_cast<int16_t *>(ctx->ws + lp.off_kstar);
-    int32_t *stats = d_stats + 4 * (l - 1);
+    int32_t *stats = d_stats + BMLP_STATS_STRIDE * (l - 1);
     LossSelectArgs ls{};
     ls.c = p.c;
     ls.z = z; ls.ldz = p.ldz;
@@ -472,7 +474,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
       c.ksteps = lp.ldq_out / 64; c.thr = lp.robust_thr;
       c.yhat = yh + (size_t)(l - 1) * p.max_batch * p.c;
       c.err = ctx->ws + lp.off_err; c.upd = ctx->ws + lp.off_upd;
-      c.stats = d_stats + 4 * (l - 1);
+      c.stats = d_stats + BMLP_STATS_STRIDE * (l - 1);
       if (cb.nl == kMaxClsLayers || l == p.L) {
         BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_cls_fp4(cb, s));
         cb.nl = 0;
@@ -495,7 +497,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
     u.kstar = reinterpret_cast<const int16_t *>(ctx->ws + lp.off_kstar);
     u.upd = ctx->ws + lp.off_upd;
     u.P = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p);
-    u.stats = d_stats + 4 * (l - 1);
+    u.stats = d_stats + BMLP_STATS_STRIDE * (l - 1);
     u.ld_h = lp.ld_h; u.nw32 = 2 * lp.words_in; u.words_out = lp.words_out;
     u.k_in = lp.k_in; u.groups = lp.groups; u.gamma = lp.gamma;
     const uint64_t T = reinforce_threshold(p_r, lp.k_out);

@@ -152,15 +152,16 @@ __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
       }
     }
   }
-  // one global atomic per counter and work-group: same-address atomics from
-  // every pattern would serialise in L2
+  // one global atomic per work-group (same-address atomics from every
+  // pattern would serialise in L2): err and |M| are adjacent 32-bit counts of
+  // the layer's stats row, added at once as one 64-bit value
   __syncthreads();
   if (tid == 0) {
     if (p.mode == kClsEval) {
       if (cnt[2]) atomicAdd(Lr.correct, cnt[2]);
     } else {
-      if (cnt[0]) atomicAdd(Lr.stats + 0, cnt[0]);
-      if (cnt[1]) atomicAdd(Lr.stats + 1, cnt[1]);
+      const unsigned long long v = (unsigned long long)(uint32_t)cnt[0] | ((unsigned long long)(uint32_t)cnt[1] << 32);
+      if (v) atomicAdd(reinterpret_cast<unsigned long long *>(Lr.stats), v);
     }
   }
 }

@@ -284,7 +284,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   nsel = wave_sum(nsel);
   if (lane == 0 && nsel) atomicAdd(&s_sel, nsel);
   __syncthreads();
-  if (tid == 0 && s_sel) atomicAdd(U.stats + 2, s_sel);   // |U_l|
+
   {
     // exclusive prefix sum of the bucket sizes: thread t owns buckets
     // [t ch, t ch + ch); a scan inside each wave, then across the waves
@@ -450,7 +450,10 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   if (tid == 0) {
     int t = 0;
     for (int w = 0; w < kWaves; ++w) t += wsum[w];
-    if (t) atomicAdd(U.stats + 3, t);   // one atomic per work-group
+    // |U_l| and the reinforced draws are adjacent 32-bit counts of the
+    // layer's stats row: one 64-bit atomic per work-group adds both
+    const unsigned long long v = (unsigned long long)(uint32_t)s_sel | ((unsigned long long)(uint32_t)t << 32);
+    if (v) atomicAdd(reinterpret_cast<unsigned long long *>(U.stats + 2), v);
   }
 }
 

@@ -113,3 +113,11 @@ def test_null_and_misaligned_buffers_rejected():
     assert L.bmlp_train_step(None, 1 << 20, 1 << 21, 4, 0, 0.5, 1 << 22, None) == B.BMLP_EINVAL
     assert L.bmlp_pack(None, 4, 10, None, None) == B.BMLP_EINVAL
     assert L.bmlp_pack(None, 0, 0, None, None) == B.BMLP_ESHAPE
+
+
+def test_stats_stride_matches_binding():
+    """The binding allocates step statistics with the header's row stride."""
+    hdr = open(os.path.join(ROOT, "include", "bmlp.h")).read()
+    m = re.search(r"#define\s+BMLP_STATS_STRIDE\s+(\d+)", hdr)
+    assert m and int(m.group(1)) == B.STATS_STRIDE
+    assert B.STATS_STRIDE * 4 % 128 == 0    # a 128-byte line per layer
