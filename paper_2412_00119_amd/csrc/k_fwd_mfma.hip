@@ -331,25 +331,28 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   }
 }
 
-// bit rows [R][words] -> fp4 rows [R][ldq]; one thread per output dword
-// (8 columns).  Also zeroes `zero[0..nzero)` (the step statistics).
+// bit rows [R][words] -> fp4 rows [R][ldq]; one thread per 16 output bytes
+// (32 columns, one 32-bit word of bits).  Also zeroes `zero[0..nzero)` (the
+// step statistics).
 __global__ __launch_bounds__(256) void fp4_rows_kernel(const uint64_t *__restrict__ bits, int words,
                                                        int K, int R, uint8_t *__restrict__ q, int ldq,
                                                        int32_t *zero, int nzero) {
-  const int dw_per_row = ldq >> 2;
+  const int per_row = ldq >> 4;   // ldq is a multiple of 64
   const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
   if (zero != nullptr && t < nzero) zero[t] = 0;
-  if (t >= (long long)R * dw_per_row) return;
-  const int r = (int)(t / dw_per_row), d = (int)(t % dw_per_row);
-  const int c0 = d * 8;                       // first column of this dword
+  if (t >= (long long)R * per_row) return;
+  const int r = (int)(t / per_row), d = (int)(t % per_row);
+  const int c0 = d * 32;                       // first column of these 16 bytes
   uint32_t b = 0u, valid = 0u;
   if (c0 < K) {
-    const uint64_t w = bits[(size_t)r * words + (c0 >> 6)];
-    b = (uint32_t)(w >> (c0 & 63)) & 0xFFu;
-    const int nv = min(K - c0, 8);
-    valid = (1u << nv) - 1u;
+    b = reinterpret_cast<const uint32_t *>(bits + (size_t)r * words)[c0 >> 5];
+    const int nv = min(K - c0, 32);
+    valid = nv == 32 ? 0xFFFFFFFFu : ((1u << nv) - 1u);
   }
-  reinterpret_cast<uint32_t *>(q + (size_t)r * ldq)[d] = fp4_from_bits8(b, valid);
+  uint32_t o[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) o[i] = fp4_from_bits8(b >> (8 * i), valid >> (8 * i));
+  reinterpret_cast<uint4 *>(q + (size_t)r * ldq)[d] = make_uint4(o[0], o[1], o[2], o[3]);
 }
 
 }  // namespace
@@ -375,7 +378,7 @@ hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s) {
 
 hipError_t launch_fp4_rows(const uint64_t *bits, int words, int K, int R, uint8_t *q, int ldq,
                            int32_t *zero, int nzero, hipStream_t s) {
-  const long long total = (long long)R * (ldq >> 2);
+  const long long total = (long long)R * (ldq >> 4);
   const long long need = total > nzero ? total : nzero;
   if (need <= 0) return hipSuccess;
   hipLaunchKernelGGL(fp4_rows_kernel, dim3((unsigned)((need + 255) / 256)), dim3(256), 0, s, bits, words,
