@@ -174,6 +174,8 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
     wo = align256(wo + (size_t)nb * lp.groups * 2);
     lp.off_aq = wo;
     wo = align256(wo + (size_t)nb * lp.ldq_out);
+    lp.off_rho = wo;   // rho^{y^mu} rows [max_batch][words_out] for the fused selection
+    wo = align256(wo + (size_t)nb * lp.words_out * 8);
   }
   p->ldq0 = fp4_row_bytes(p->widths[0]);
   p->off_xq = wo;
@@ -410,10 +412,30 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
   int16_t *z = reinterpret_cast<int16_t *>(ctx->ws + p.off_z);
   int32_t *yh = reinterpret_cast<int32_t *>(ctx->ws + p.off_yhat);
   uint8_t *xq = ctx->ws + p.off_xq;
-  if (mfma)   // input as fp4 rows; also zeroes the statistics
-    BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s,
-               launch_fp4_rows(d_x, p.layer[0].words_in, p.widths[0], n, xq, p.ldq0, d_stats,
-                               BMLP_STATS_STRIDE * p.L, s));
+  if (mfma) {
+    // input as fp4 rows, statistics zeroed, and the rho^{y^mu} rows of every
+    // layer whose selection is fused into its forward
+    PrepArgs pa{};
+    pa.x = d_x; pa.words = p.layer[0].words_in; pa.K = p.widths[0]; pa.n = n;
+    pa.xq = xq; pa.ldq = p.ldq0;
+    pa.zero = d_stats; pa.nzero = BMLP_STATS_STRIDE * p.L;
+    pa.y = d_y; pa.c = p.c;
+    for (int l = 1; l <= p.L; ++l) {
+      const LayerPlan &lp = p.layer[l - 1];
+      if (lp.gamma == 64) {
+        PrepLayer &q = pa.L[pa.nl++];
+        q.P = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p);
+        q.rho = reinterpret_cast<uint64_t *>(ctx->ws + lp.off_rho);
+        q.words_out = lp.words_out;
+      }
+      if (pa.nl == kMaxPrepLayers || (l == p.L && (pa.nl > 0 || pa.xq != nullptr))) {
+        BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s, launch_step_prep(pa, s));
+        pa.xq = nullptr;   // the input and the statistics are done by the first launch
+        pa.zero = nullptr; pa.nzero = 0;
+        pa.nl = 0;
+      }
+    }
+  }
   const uint64_t *a_prev = d_x;
   const uint8_t *aq_prev = xq;
   for (int l = 1; l <= p.L; ++l) {
@@ -443,7 +465,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
       f.afp4 = ctx->ws + lp.off_aq; f.ld_af = lp.ldq_out;
       f.mode = fused ? kFwdFusedSelect : kFwdWriteZ;
       f.kstar = kstar; f.ldk = p.max_batch;
-      f.y = d_y; f.Pbits = P; f.c = p.c;
+      f.rho = reinterpret_cast<const uint64_t *>(ctx->ws + lp.off_rho); f.ldr = lp.words_out;
       f.z = z; f.ldz = p.ldz;
       BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s, launch_fwd_fp4(f, s));
       if (!fused) {   // Algorithm 2 from the stored z, before the next layer reuses it

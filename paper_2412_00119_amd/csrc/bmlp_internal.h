@@ -24,7 +24,7 @@ struct LayerPlan {
   int robust_thr;            // ceil(r K_l)
   int ldq_in, ldq_out;       // bytes per fp4 row of K_{l-1} / K_l elements
   size_t off_h, off_w, off_p, off_wq, off_pq;     // state
-  size_t off_a, off_err, off_upd, off_kstar, off_aq;   // workspace
+  size_t off_a, off_err, off_upd, off_kstar, off_aq, off_rho;   // workspace
 };
 
 struct Plan {
@@ -80,16 +80,32 @@ struct FwdArgs {
   uint8_t *afp4; int ld_af;         // a_l fp4 [M][ld_af]
   int mode;
   int16_t *kstar; int ldk;          // kFwdFusedSelect (gamma = 64): raw selection [groups][ldk]
-  const int32_t *y; const uint64_t *Pbits; int c;
+  const uint64_t *rho; int ldr;     // kFwdFusedSelect: rho^{y^mu} rows [M][ldr]
   int16_t *z; int ldz;              // kFwdWriteZ
   int nt_m, nt_n, xcd_remap;        // set by the launcher
-  int ldp, pw_max;                  // set by the launcher: Pbits row stride and last word
+  int pw_max;                       // set by the launcher: last word of a rho row
 };
 hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s);
 
 // bit rows [R][words] of K columns -> fp4 rows [R][ldq]; also zeroes zero[0..nzero)
 hipError_t launch_fp4_rows(const uint64_t *bits, int words, int K, int R, uint8_t *q, int ldq,
                            int32_t *zero, int nzero, hipStream_t s);
+
+// The start of a matrix-core train step, in one launch: the input as fp4
+// rows, the statistics zeroed, and for each listed layer the rows
+// rho^{y^mu} of P_l for every pattern (for the forward's fused selection).
+constexpr int kMaxPrepLayers = 8;
+struct PrepLayer {
+  const uint64_t *P; uint64_t *rho; int words_out;   // rho [n][words_out]
+};
+struct PrepArgs {
+  const uint64_t *x; int words, K, n;   // input bit rows [n][words]
+  uint8_t *xq; int ldq;                 // input fp4 rows [n][ldq]; null: skip
+  int32_t *zero; int nzero;
+  const int32_t *y; int c;
+  PrepLayer L[kMaxPrepLayers]; int nl;
+};
+hipError_t launch_step_prep(const PrepArgs &a, hipStream_t s);
 
 // Classifier on the matrix cores, then the local error signal, for up to
 // kMaxClsLayers layers in one launch (ceil(n / 16) work-groups per layer).

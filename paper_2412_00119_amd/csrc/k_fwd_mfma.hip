@@ -22,6 +22,8 @@
 //   * for any other gamma, z as int16 for the generic selection kernel.
 // Work-groups are mapped so that each XCD (work-group id mod 8) works on
 // its own slice of W_l, which then stays in that XCD's L2.
+#include <algorithm>
+
 #include "bmlp_internal.h"
 #include "fp4.h"
 
@@ -98,16 +100,16 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   const int m0 = mt * TM, n0 = nt * TN;
 
   // For the fused selection: thread (r, w) fetches word w of the tile's
-  // columns of rho^{y^mu} for tile row r (pattern m0 + r), before the
-  // operand loads start (the compiler does not count direct-to-LDS loads, so
-  // a register load issued among them would make it wait for all of them).
-  // The loads are unconditional (indices clamped; when the selection is not
-  // fused the launcher points them at valid memory with a zero row stride).
+  // columns of rho^{y^mu} for tile row r (pattern m0 + r) from the rows
+  // gathered at the start of the step, before the operand loads start (the
+  // compiler does not count direct-to-LDS loads, so a register load issued
+  // among them would make it wait for all of them).  The load is
+  // unconditional (indices clamped; when the selection is not fused the
+  // launcher points it at valid memory with a zero row stride).
   const int pr = tid >> 1, pw = tid & 1;
   const int pm = m0 + pr, pwg = (n0 >> 6) + pw;
   const bool pvalid = p.mode == kFwdFusedSelect && pm < p.M && pwg < p.words_out;
-  const int yl = min(max(p.y[min(pm, p.M - 1)], 0), p.c - 1);
-  const uint64_t prow = p.Pbits[(size_t)yl * p.ldp + min(pwg, p.pw_max)];
+  const uint64_t prow = p.rho[(size_t)min(pm, p.M - 1) * p.ldr + min(pwg, p.pw_max)];
   __builtin_amdgcn_sched_barrier(0);
 
   // Loads: a wave moves rows 32*wave .. 32*wave+31 of each operand, 16 rows
@@ -355,6 +357,36 @@ __global__ __launch_bounds__(256) void fp4_rows_kernel(const uint64_t *__restric
   reinterpret_cast<uint4 *>(q + (size_t)r * ldq)[d] = make_uint4(o[0], o[1], o[2], o[3]);
 }
 
+// blockIdx.y = 0: input fp4 rows (and the statistics zeroed); 1 + i: the
+// rho rows of layer i of the batch, one thread per 64-bit word.
+__global__ __launch_bounds__(256) void step_prep_kernel(PrepArgs p) {
+  const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (blockIdx.y == 0) {
+    if (p.zero != nullptr && t < p.nzero) p.zero[t] = 0;
+    if (p.xq == nullptr) return;
+    const int per_row = p.ldq >> 4;
+    if (t >= (long long)p.n * per_row) return;
+    const int r = (int)(t / per_row), d = (int)(t % per_row);
+    const int c0 = d * 32;
+    uint32_t b = 0u, valid = 0u;
+    if (c0 < p.K) {
+      b = reinterpret_cast<const uint32_t *>(p.x + (size_t)r * p.words)[c0 >> 5];
+      const int nv = min(p.K - c0, 32);
+      valid = nv == 32 ? 0xFFFFFFFFu : ((1u << nv) - 1u);
+    }
+    uint32_t o[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[i] = fp4_from_bits8(b >> (8 * i), valid >> (8 * i));
+    reinterpret_cast<uint4 *>(p.xq + (size_t)r * p.ldq)[d] = make_uint4(o[0], o[1], o[2], o[3]);
+    return;
+  }
+  const PrepLayer &L = p.L[blockIdx.y - 1];
+  if (t >= (long long)p.n * L.words_out) return;
+  const int mu = (int)(t / L.words_out), w = (int)(t % L.words_out);
+  const int yl = min(max(p.y[mu], 0), p.c - 1);   // stay inside P on a bad label
+  L.rho[t] = L.P[(size_t)yl * L.words_out + w];
+}
+
 }  // namespace
 
 hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s) {
@@ -363,13 +395,10 @@ hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s) {
   a.nt_n = (a.N + TN - 1) / TN;
   a.xcd_remap = (a.nt_n % 8 == 0) ? 1 : 0;
   if (a.mode == kFwdFusedSelect) {
-    a.ldp = a.words_out;
     a.pw_max = a.words_out - 1;
-  } else {   // the kernel's label / classifier loads read A instead (always valid)
-    a.y = reinterpret_cast<const int32_t *>(a.A);
-    a.Pbits = reinterpret_cast<const uint64_t *>(a.A);
-    a.c = 1;
-    a.ldp = 0;
+  } else {   // the kernel's rho load reads A instead (always valid)
+    a.rho = reinterpret_cast<const uint64_t *>(a.A);
+    a.ldr = 0;
     a.pw_max = 0;
   }
   hipLaunchKernelGGL(fwd_fp4_kernel, dim3(a.nt_m * a.nt_n), dim3(256), 0, s, a);
@@ -385,5 +414,15 @@ hipError_t launch_fp4_rows(const uint64_t *bits, int words, int K, int R, uint8_
                      K, R, q, ldq, zero, nzero);
   return hipGetLastError();
 }
+
+hipError_t launch_step_prep(const PrepArgs &a, hipStream_t s) {
+  long long need = a.nzero;
+  if (a.xq != nullptr) need = std::max(need, (long long)a.n * (a.ldq >> 4));
+  for (int i = 0; i < a.nl; ++i) need = std::max(need, (long long)a.n * a.L[i].words_out);
+  if (need <= 0) return hipSuccess;
+  hipLaunchKernelGGL(step_prep_kernel, dim3((unsigned)((need + 255) / 256), 1 + a.nl), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 
 }  // namespace bmlp
