@@ -44,6 +44,15 @@ __device__ __forceinline__ void dma16(const void *src, void *dst_wave_base) {
   __builtin_amdgcn_global_load_lds(src, (lds_void *)dst_wave_base, 16, 0, 0);
 }
 
+// v_writelane_b32: lane `lane` of the result takes the wave-uniform value
+// `v`, every other lane keeps `old` (the compiler intrinsic, which this
+// clang exposes under its LLVM name only)
+extern "C" __device__ uint32_t bmlp_llvm_writelane(uint32_t v, uint32_t lane, uint32_t old)
+    __asm("llvm.amdgcn.writelane.i32");
+__device__ __forceinline__ uint32_t lane_write(uint32_t old, uint32_t v, int lane) {
+  return bmlp_llvm_writelane(v, (uint32_t)lane, old);
+}
+
 // wait until at most n vector-memory operations of this wave are outstanding
 template <int N>
 __device__ __forceinline__ void wait_vm() {
@@ -227,21 +236,47 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   // ---- epilogue ---------------------------------------------------------------
   // lane holds z for column n0 + wn*64 + j*32 + (lane & 31) and rows
   // m0 + wm*64 + i*32 + 8*(e >> 2) + 4*(lane >> 5) + (e & 3) in acc[i][j][e]
-  uint32_t *sbits = reinterpret_cast<uint32_t *>(s0);   // [128 rows][4 chunks of 32 columns]
   const int lh = lane >> 5, lc = lane & 31;
+  // a_l = sign(z): the ballot of (i, j, e) holds the signs of 32 columns
+  // (half j of the wave's 64) of two rows (lanes 0-31 and 32-63).  Ballot
+  // k = 16 (2i + j) + e is moved to lane k, which then writes both rows' 32
+  // bits and their fp4 form: no LDS round trip, four stores per lane.
+  uint32_t blo = 0u, bhi = 0u;
+  uint64_t colok[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) colok[j] = __ballot(n0 + wn * 64 + j * 32 + lc < p.N);
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int col = n0 + wn * 64 + j * 32 + lc;
-        const uint64_t bal = __ballot(col < p.N && acc[i][j][e] >= 0.f);
-        if (lc == 0) {
-          const int rl = wm * 64 + i * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
-          sbits[rl * 4 + wn * 2 + j] = (uint32_t)(bal >> (32 * lh));
-        }
+        const uint64_t bal = __ballot(acc[i][j][e] >= 0.f) & colok[j];
+        const int k = (2 * i + j) * 16 + e;
+        blo = lane_write(blo, (uint32_t)bal, k);
+        bhi = lane_write(bhi, (uint32_t)(bal >> 32), k);
       }
+  {
+    const int i = lane >> 5, j = (lane >> 4) & 1, e = lane & 15;
+    const int rl0 = wm * 64 + i * 32 + 8 * (e >> 2) + (e & 3);   // the lanes-0-31 row; +4 for 32-63
+    const int cb = n0 + wn * 64 + j * 32;                          // first of the 32 columns
+    const int nv = min(max(p.N - cb, 0), 32);
+    const uint32_t valid = nv == 32 ? 0xFFFFFFFFu : ((1u << nv) - 1u);
+    uint32_t *ab32 = reinterpret_cast<uint32_t *>(p.abits);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int m = m0 + rl0 + 4 * h;
+      const uint32_t bits = h ? bhi : blo;
+      if (m < p.M) {
+        // the bit row's 32-bit half (columns past N are 0 in the ballot)
+        if ((cb >> 5) < 2 * p.words_out) ab32[(size_t)m * 2 * p.words_out + (cb >> 5)] = bits;
+        uint32_t o[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] = fp4_from_bits8(bits >> (8 * q), valid >> (8 * q));
+        *reinterpret_cast<uint4 *>(p.afp4 + (size_t)m * p.ld_af + (cb >> 1)) = make_uint4(o[0], o[1], o[2], o[3]);
+      }
+    }
+  }
 
   if (p.mode == kFwdFusedSelect) {
     const int gcol0 = n0 + wn * 64;   // the wave's 64 columns are one group
@@ -301,35 +336,6 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
           const int col = n0 + wn * 64 + j * 32 + lc;
           if (m < p.M && col < p.N) p.z[(size_t)m * p.ldz + col] = (int16_t)(int)acc[i][j][e];
         }
-  }
-  __syncthreads();
-
-  // a_l bits: 128 rows x 2 words
-  {
-    const int r = tid >> 1, w = tid & 1;
-    const int m = m0 + r, wg = (n0 >> 6) + w;
-    if (m < p.M && wg < p.words_out) {
-      const uint64_t v = *reinterpret_cast<const uint64_t *>(&sbits[r * 4 + w * 2]);
-      p.abits[(size_t)m * p.words_out + wg] = v;
-    }
-  }
-  // a_l fp4: 128 rows x 64 bytes; a thread converts 64 columns (32 bytes)
-  {
-    const int r = tid >> 1, h = tid & 1;
-    const int m = m0 + r;
-    if (m < p.M) {
-      const uint64_t bits = *reinterpret_cast<const uint64_t *>(&sbits[r * 4 + h * 2]);
-      const int cbase = n0 + h * 64;
-      const int nv = min(max(p.N - cbase, 0), 64);
-      const uint64_t valid = nv == 64 ? ~0ull : ((1ull << nv) - 1ull);
-      uint32_t o[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q)
-        o[q] = fp4_from_bits8((uint32_t)(bits >> (8 * q)), (uint32_t)(valid >> (8 * q)));
-      uint4 *dst = reinterpret_cast<uint4 *>(p.afp4 + (size_t)m * p.ld_af + (cbase >> 1));
-      dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
-      dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
-    }
   }
 }
 
