@@ -82,6 +82,19 @@ __device__ __forceinline__ v16f mfma_fp4(const uint4 &a, const uint4 &b, v16f c)
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, c, 4, 4, 0, 127, 0, 127);
 }
 
+// one reduce-scatter step at lane distance D, the partner given by DPP
+// control CTRL: rows k + D move into slot k on lanes with bit D set
+template <int D, int CTRL>
+__device__ __forceinline__ void select_step(uint32_t (&v)[32], int lc) {
+  const bool up = (lc & D) != 0;
+#pragma unroll
+  for (int k = 0; k < D; ++k) {
+    const uint32_t send = up ? v[k] : v[k + D];
+    const uint32_t keep = up ? v[k + D] : v[k];
+    v[k] = min(keep, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)send, CTRL, 0xF, 0xF, false));
+  }
+}
+
 __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   // one LDS array per ring slot (A tile, then B tile): every access below
   // names its array, so the compiler can tell a slot being read from the
@@ -89,7 +102,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   // eight such arrays).  66 KB in all: two work-groups fit on a CU.
   constexpr int kSlot = (TM + TN) * KB;
   __shared__ __align__(16) uint8_t s0[kSlot], s1[kSlot], s2[kSlot], s3[kSlot];
-  __shared__ uint64_t sP[TM][2];       // rho^{y^mu} bits of the tile's 128 columns
+  __shared__ uint64_t sP[2][TM];       // rho^{y^mu} bits of the tile's 128 columns, per group
   static_assert(kStages == 4, "one named array per slot");
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -230,7 +243,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     if (ks + 2 < nks) step(ks + 2, r0, r1, s3, s1);
   }
   wait_vm<0>();   // the repeated loads of the last steps have landed
-  sP[pr][pw] = pvalid ? prow : 0ull;
+  sP[pw][pr] = pvalid ? prow : 0ull;
   __syncthreads();
 
   // ---- epilogue ---------------------------------------------------------------
@@ -282,48 +295,53 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     const int gcol0 = n0 + wn * 64;   // the wave's 64 columns are one group
     if (gcol0 < p.N) {
       const int g = gcol0 >> 6;
-      // key of each of the lane's 32 rows q = 16*i + e over its 2 columns
+      // Key of each of the lane's 32 rows q = 16*i + e over its 2 columns,
+      // formed on the bits of the exact fp32 z: with s = -z where the
+      // classifier weight is +1 and s = z where it is -1, perceptron k is
+      // wrong iff s >= 1, and t = s - 0.5 is then positive with |z| - 0.5 in
+      // its magnitude (at most 16 significant bits, as |z| <= K_{l-1} <=
+      // 32767, so the low 8 bits are zero and take the column).  Unsigned
+      // order of bits(t) | k is (|z|, k) over the wrong perceptrons, and
+      // every right one (t < 0, sign bit set) comes after them.
+      const uint32_t sh = 31u - (uint32_t)lc;
       uint32_t v[32];
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int rl = wm * 64 + i * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
-          const uint64_t rho = sP[rl][wn];
-          uint32_t key = 0xFFFFFFFFu;
+          const uint64_t rho = sP[wn][rl];
+          uint32_t key[2];
 #pragma unroll
           for (int j = 0; j < 2; ++j) {
-            const int kl = j * 32 + lc;              // column within the group
-            const int zz = (int)acc[i][j][e];
-            const bool rpos = (rho >> kl) & 1ull;
-            const bool wrong = rpos ? (zz < 0) : (zz > 0);
-            const uint32_t kk = ((uint32_t)(zz < 0 ? -zz : zz) << 8) | (uint32_t)kl;
-            key = wrong ? min(key, kk) : key;
+            const uint32_t r = (uint32_t)(rho >> (32 * j)) << sh;   // bit 31: rho of column j*32 + lc
+            const float sz = __uint_as_float(__float_as_uint(acc[i][j][e]) ^ (r & 0x80000000u));
+            key[j] = __float_as_uint(sz - 0.5f) | (uint32_t)(j * 32 + lc);
           }
-          v[i * 16 + e] = key;
+          v[i * 16 + e] = min(key[0], key[1]);
         }
-      // butterfly reduce-scatter over the 32 lanes of a half-wave: at distance
-      // d a lane keeps half of its rows (the upper half if bit d of its lane
-      // is set) and takes the minimum with the partner's copy of those rows;
-      // afterwards lane lc holds the minimum over all 64 columns of row q = lc
+      // Reduce-scatter over the 32 lanes of a half-wave: at each step a lane
+      // keeps half of its rows (the upper half if the step's lane bit is
+      // set) and takes the minimum with a partner's copy of those rows.
+      // Lane bit 4: v_permlane16_swap trades the odd 16-lane rows of its
+      // first operand for the even rows of its second, which leaves each
+      // lane its own and its partner's copy of the rows it keeps.  Bits 3..0:
+      // DPP row_mirror, row_half_mirror and two quad permutations, each of
+      // which pairs a lane with one that differs in that bit.  Afterwards
+      // lane lc holds the minimum over all 64 columns of row q = lc.
 #pragma unroll
-      for (int d = 16; d >= 1; d >>= 1) {
-        const uint32_t upm = (lc & d) ? 0xFFFFFFFFu : 0u;
-#pragma unroll
-        for (int k = 0; k < d; ++k) {
-          // swap v[k], v[k+d] on upper lanes with a mask (no selects between
-          // array elements, which the compiler would turn into indexing)
-          const uint32_t x = (v[k] ^ v[k + d]) & upm;
-          const uint32_t send = v[k + d] ^ x;
-          const uint32_t keep = v[k] ^ x;
-          const uint32_t recv = (uint32_t)__shfl_xor((int)send, d, 64);
-          v[k] = min(keep, recv);
-        }
+      for (int k = 0; k < 16; ++k) {
+        const auto sw = __builtin_amdgcn_permlane16_swap(v[k], v[k + 16], false, false);
+        v[k] = min((uint32_t)sw[0], (uint32_t)sw[1]);
       }
+      select_step<8, 0x140>(v, lc);   // row_mirror: lane i <-> 15 - i
+      select_step<4, 0x141>(v, lc);   // row_half_mirror: lane i <-> 7 - i
+      select_step<2, 0x4E>(v, lc);    // quad_perm [2,3,0,1]
+      select_step<1, 0xB1>(v, lc);    // quad_perm [1,0,3,2]
       const int i = lc >> 4, e = lc & 15;
       const int rl = wm * 64 + i * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
       const int m = m0 + rl;
-      if (m < p.M) p.kstar[(size_t)g * p.ldk + m] = v[0] == 0xFFFFFFFFu ? (int16_t)-1 : (int16_t)(v[0] & 0xFFu);
+      if (m < p.M) p.kstar[(size_t)g * p.ldk + m] = (v[0] >> 31) ? (int16_t)-1 : (int16_t)(v[0] & 0x3Fu);
     }
   } else if (p.mode == kFwdWriteZ) {
 #pragma unroll
