@@ -5,13 +5,15 @@
 //
 // A work-group owns 16 patterns of one layer and all classes, taken CB
 // blocks of 16 classes per pass (CB is a template parameter sized to the
-// class count).  Its sixteen waves split K (wave w takes K steps w, w+16,
-// ...); for each step a wave loads its operands, waits and runs one
-// v_mfma_scale_f32_16x16x128_f8f6f4 per class block, and the other fifteen
-// waves on the CU hide that latency.  Loads are unconditional (indices
-// clamped, data masked).  The partial sums are exact integers, so they are
-// converted to int32 and added with integer LDS atomics (float LDS atomics
-// are far slower), giving the same y_hat in any order.
+// class count).  Its sixteen waves form KG groups along K times 16 / KG
+// groups along the classes: a wave runs one
+// v_mfma_scale_f32_16x16x128_f8f6f4 per K step for each of its PB class
+// blocks, over K steps kg, kg + KG, ..., with the operands of kU steps
+// loaded together so that one memory latency covers them.  Loads are
+// unconditional with clamped indices: a clamped row only feeds y_hat
+// entries of patterns past n or classes past c, which are never read.  The partial sums are exact
+// integers: each K group stores its int32 partials in LDS and every thread
+// then adds the KG partials of its own y_hat entries, in a fixed order.
 //
 // Then each wave takes one pattern: first argmax (lowest class on ties), the
 // two largest values (tau = top1 - top2, 0 on a tie), err = (pred != y) and
@@ -35,10 +37,6 @@ __device__ __forceinline__ v4f mfma_fp4(const uint4 &a, const uint4 &b, v4f c) {
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(av, bv, c, 4, 4, 0, 127, 0, 127);
 }
 
-__device__ __forceinline__ uint4 masked(const uint4 &v, uint32_t m) {
-  return make_uint4(v.x & m, v.y & m, v.z & m, v.w & m);
-}
-
 struct Top2 {
   int v1, i1, v2;
 };
@@ -57,11 +55,21 @@ __device__ __forceinline__ Top2 merge(Top2 a, Top2 b) {
 }
 
 template <int CB>
+struct ClsShape {
+  static constexpr int PB = CB < 4 ? CB : 4;     // class blocks per wave
+  static constexpr int CG = CB / PB;             // wave groups along the classes
+  static constexpr int KG = kWaves / CG;         // wave groups along K
+  static constexpr int kU = KG >= 16 ? 2 : 4;    // K steps loaded together
+};
+
+template <int CB>
 __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
-  __shared__ int red[16][CB * 16];
-  __shared__ int cnt[3];   // block totals of err, upd, correct
+  constexpr int PB = ClsShape<CB>::PB, KG = ClsShape<CB>::KG, kU = ClsShape<CB>::kU;
+  __shared__ int red[KG][16][CB * 16];   // per K group; red[0] ends with y_hat
+  __shared__ int cnt[3];                 // block totals of err, upd, correct
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int kg = wave % KG, cg = wave / KG;
   const int bpl = (p.n + 15) / 16;               // work-groups per layer
   const ClsLayer &Lr = p.L[blockIdx.x / bpl];
   const int m0 = (blockIdx.x % bpl) * 16;
@@ -69,46 +77,60 @@ __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
   const int nblk = (p.c + 15) / 16;
   const bool one_pass = nblk <= CB;
   const int am = m0 + lr;
-  const uint32_t amask = am < p.n ? 0xFFFFFFFFu : 0u;
-  const uint8_t *arow = Lr.A + (size_t)min(am, p.n - 1) * Lr.lda + lk;
+  // 32-bit byte offsets from the layer's base pointers (scalar base +
+  // vector offset addressing; a_l and P_l are far below 4 GiB)
+  const uint32_t aoff = (uint32_t)min(am, p.n - 1) * (uint32_t)Lr.lda + (uint32_t)lk;
+  const int ksteps = Lr.ksteps;
   if (tid < 3) cnt[tid] = 0;
 
   for (int cb0 = 0; cb0 < nblk; cb0 += CB) {
     const int nb = min(CB, nblk - cb0);
-    for (int i = tid; i < 16 * CB * 16; i += 64 * kWaves) (&red[0][0])[i] = 0;
-    v4f acc[CB];
+    v4f acc[PB];
+    uint32_t boff[PB];
 #pragma unroll
-    for (int j = 0; j < CB; ++j) acc[j] = (v4f){0.f, 0.f, 0.f, 0.f};
-    const uint8_t *brow[CB];
-    uint32_t bmask[CB];
-#pragma unroll
-    for (int j = 0; j < CB; ++j) {
-      const int cls = (cb0 + j) * 16 + lr;
-      bmask[j] = cls < p.c ? 0xFFFFFFFFu : 0u;
-      brow[j] = Lr.P + (size_t)min(cls, p.c - 1) * Lr.ldp + lk;
+    for (int j = 0; j < PB; ++j) {
+      acc[j] = (v4f){0.f, 0.f, 0.f, 0.f};
+      const int cls = (cb0 + cg * PB + j) * 16 + lr;
+      boff[j] = (uint32_t)min(cls, p.c - 1) * (uint32_t)Lr.ldp + (uint32_t)lk;
     }
-    for (int ks = wave; ks < Lr.ksteps; ks += kWaves) {
-      const uint4 a = masked(*reinterpret_cast<const uint4 *>(arow + ks * 64), amask);
-      uint4 b[CB];
+    const bool any = cg * PB < nb;   // wave-uniform: the wave has a class block in range
+    for (int ks0 = kg; any && ks0 < ksteps; ks0 += KG * kU) {
+      uint4 a[kU], b[kU][PB];
 #pragma unroll
-      for (int j = 0; j < CB; ++j) b[j] = *reinterpret_cast<const uint4 *>(brow[j] + ks * 64);
+      for (int u = 0; u < kU; ++u) {
+        const int ks = min(ks0 + u * KG, ksteps - 1);
+        a[u] = *reinterpret_cast<const uint4 *>(Lr.A + (aoff + (uint32_t)ks * 64u));
 #pragma unroll
-      for (int j = 0; j < CB; ++j)
-        if (j < nb) acc[j] = mfma_fp4(a, masked(b[j], bmask[j]), acc[j]);
+        for (int j = 0; j < PB; ++j) b[u][j] = *reinterpret_cast<const uint4 *>(Lr.P + (boff[j] + (uint32_t)ks * 64u));
+      }
+#pragma unroll
+      for (int u = 0; u < kU; ++u)
+        if (ks0 + u * KG < ksteps) {
+#pragma unroll
+          for (int j = 0; j < PB; ++j)
+            if (cg * PB + j < nb) acc[j] = mfma_fp4(a[u], b[u][j], acc[j]);
+        }
     }
-    __syncthreads();   // red is zeroed
-    // lane holds classes (cb0 + j)*16 + (lane & 15) of patterns 4*(lane >> 4) + e
+    // lane holds classes (cb0 + cg*PB + j)*16 + (lane & 15) of patterns
+    // 4*(lane >> 4) + e; blocks past nb are never read
 #pragma unroll
-    for (int j = 0; j < CB; ++j)
-      if (j < nb)
+    for (int j = 0; j < PB; ++j)
+      if (cg * PB + j < nb)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) atomicAdd(&red[4 * (lane >> 4) + e][j * 16 + lr], (int)acc[j][e]);
+        for (int e = 0; e < 4; ++e) red[kg][4 * (lane >> 4) + e][(cg * PB + j) * 16 + lr] = (int)acc[j][e];
+    __syncthreads();
+    for (int i = tid; i < 16 * CB * 16; i += 64 * kWaves) {
+      int sum = 0;
+#pragma unroll
+      for (int k = 0; k < KG; ++k) sum += (&red[k][0][0])[i];
+      (&red[0][0][0])[i] = sum;
+    }
     __syncthreads();
     if (!(one_pass && p.mode != kClsYhatOnly)) {
       for (int i = tid; i < 16 * CB * 16; i += 64 * kWaves) {
         const int r = i / (CB * 16), cl = i % (CB * 16);
         const int m = m0 + r, cls = cb0 * 16 + cl;
-        if (m < p.n && cls < p.c) Lr.yhat[(size_t)m * p.c + cls] = red[r][cl];
+        if (m < p.n && cls < p.c) Lr.yhat[(size_t)m * p.c + cls] = red[0][r][cl];
       }
       __syncthreads();   // y_hat of this pass is in memory (same work-group)
     }
@@ -121,7 +143,7 @@ __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
     Top2 t{INT_MIN, INT_MAX, INT_MIN};
     const int32_t *row = Lr.yhat + (size_t)mu * p.c;
     for (int cl = lane; cl < p.c; cl += 64) {
-      const int v = one_pass ? red[r][cl] : row[cl];
+      const int v = one_pass ? red[0][r][cl] : row[cl];
       if (v > t.v1) {
         t.v2 = t.v1;
         t.v1 = v;
