@@ -104,22 +104,24 @@ typedef struct bmlp_config {
  *   k_in, k_out      K_{l-1}, K_l.
  *   gamma, groups    group size and G_l = K_l / gamma.
  *   words_in/out     uint64 words per bit row of a_{l-1} / a_l.
- *   ld_h             bytes per row of H_l (one byte per column, >= k_in,
- *                    a multiple of 64).
+ *   h_planes, h_ps   H_l stores u = (h + B) / 2, an integer in [0, B] (h is
+ *                    odd), in h_planes = bits(B) bit planes (5 for B = 31,
+ *                    7 for B = 127) of h_ps 32-bit words each (h_ps >=
+ *                    ceil(k_in / 32), a multiple of 16).
+ *   ld_h             bytes per row of H_l: 4 * h_planes * h_ps.
  *   robust_thr       ceil(r * K_l), computed in IEEE double.
  *   ldq_in/out       bytes per fp4 row of K_{l-1} / K_l values (64 per 128 values).
  *   off_h, off_w, off_p  byte offsets in the state buffer of
- *                    H_l  [k_out][ld_h bytes]  int8 hidden weights, perceptron-major
+ *                    H_l  [k_out][ld_h bytes]  hidden weights, perceptron-major
  *                                                    (the transpose of the paper's
  *                                                    K_{l-1} x K_l, so h^k is a row),
- *                                                    stored bit-sliced: columns
- *                                                    32g .. 32g+31 of a row are the
- *                                                    32 bytes at 32g, read as eight
- *                                                    uint32 words; bit i of word p
- *                                                    is bit p of the two's-complement
- *                                                    value of column 32g + i.
- *                                                    Columns past k_in hold 0.
- *                                                    bmlp_read_h unpacks it;
+ *                                                    stored bit-sliced: a row is
+ *                                                    h_planes planes of h_ps uint32
+ *                                                    words; bit i of word g of plane
+ *                                                    p is bit p of u = (h + B) / 2
+ *                                                    for column 32g + i.  Columns
+ *                                                    past k_in hold u = 0.
+ *                                                    bmlp_read_h unpacks it to int8;
  *                    W_l  uint64 [k_out][words_in]   visible weights sign(H_l), bits;
  *                    P_l  uint64 [n_classes][words_out]  fixed classifier, row y is rho^y;
  *                    and, as matrix-core operands, copies of W_l (off_wq, uint8
@@ -145,6 +147,7 @@ typedef struct bmlp_layer_info {
   uint64_t off_a, off_err, off_upd, off_kstar;
   int32_t ldq_in, ldq_out;
   uint64_t off_wq, off_pq, off_aq;
+  int32_t h_planes, h_ps;
 } bmlp_layer_info;
 
 typedef struct bmlp_ctx bmlp_ctx;   /* opaque, host memory only */

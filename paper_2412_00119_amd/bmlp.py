@@ -61,7 +61,8 @@ class bmlp_layer_info(ctypes.Structure):
                [(n, ctypes.c_uint64) for n in
                 ("off_h", "off_w", "off_p", "off_a", "off_err", "off_upd", "off_kstar")] + \
                [(n, ctypes.c_int32) for n in ("ldq_in", "ldq_out")] + \
-               [(n, ctypes.c_uint64) for n in ("off_wq", "off_pq", "off_aq")]
+               [(n, ctypes.c_uint64) for n in ("off_wq", "off_pq", "off_aq")] + \
+               [(n, ctypes.c_int32) for n in ("h_planes", "h_ps")]
 
 
 _lib = None

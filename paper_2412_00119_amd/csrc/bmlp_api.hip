@@ -143,7 +143,8 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
     lp.groups = lp.k_out / lp.gamma;
     lp.words_in = words64(lp.k_in);
     lp.words_out = words64(lp.k_out);
-    lp.ld_h = 64 * lp.words_in;
+    lp.h_ps = (2 * lp.words_in + 15) / 16 * 16;
+    lp.ld_h = 4 * h_planes(p->bound) * lp.h_ps;
     lp.ldq_in = fp4_row_bytes(lp.k_in);
     lp.ldq_out = fp4_row_bytes(lp.k_out);
     const double thr = ceil(p->r * (double)lp.k_out);
@@ -293,7 +294,8 @@ int setup(const bmlp_config *cfg, void *d_state, void *d_ws, void *stream, bmlp_
     uint8_t *H = ctx->state + lp.off_h;
     uint64_t *W = reinterpret_cast<uint64_t *>(ctx->state + lp.off_w);
     uint64_t *P = reinterpret_cast<uint64_t *>(ctx->state + lp.off_p);
-    hipError_t e = launch_init_h(H, lp.ld_h, W, lp.words_in, lp.k_in, lp.k_out, p.seed, l, from_h, s);
+    hipError_t e = launch_init_h(H, lp.ld_h, lp.h_ps, p.bound, W, lp.words_in, lp.k_in, lp.k_out, p.seed, l,
+                                 from_h, s);
     if (e == hipSuccess && !from_h) e = launch_init_p(P, lp.words_out, lp.k_out, p.c, p.seed, l, s);
     // fp4 operand copies of W_l and P_l for the matrix-core path
     if (e == hipSuccess)
@@ -340,6 +342,8 @@ int bmlp_describe(const bmlp_config *cfg, int32_t l, bmlp_layer_info *info) {
   info->words_in = lp.words_in;
   info->words_out = lp.words_out;
   info->ld_h = lp.ld_h;
+  info->h_planes = h_planes(p.bound);
+  info->h_ps = lp.h_ps;
   info->robust_thr = lp.robust_thr;
   info->off_h = lp.off_h;
   info->off_w = lp.off_w;
@@ -520,7 +524,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
     u.upd = ctx->ws + lp.off_upd;
     u.P = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p);
     u.stats = d_stats + BMLP_STATS_STRIDE * (l - 1);
-    u.ld_h = lp.ld_h; u.nw32 = 2 * lp.words_in; u.words_out = lp.words_out;
+    u.ld_h = lp.ld_h; u.h_ps = lp.h_ps; u.nw32 = 2 * lp.words_in; u.words_out = lp.words_out;
     u.k_in = lp.k_in; u.groups = lp.groups; u.gamma = lp.gamma;
     const uint64_t T = reinforce_threshold(p_r, lp.k_out);
     u.t_hi = (uint32_t)(T >> 24); u.t_lo = (uint32_t)(T & 0xFFFFFFu);
@@ -547,7 +551,8 @@ int bmlp_read_h(bmlp_ctx *ctx, int32_t l, int8_t *d_out, void *stream) {
   if (ctx == nullptr || d_out == nullptr) return BMLP_EINVAL;
   if (l < 1 || l > ctx->plan.L) return BMLP_ESHAPE;
   const LayerPlan &lp = ctx->plan.layer[l - 1];
-  BMLP_LAUNCH(launch_read_h(ctx->state + lp.off_h, lp.ld_h, lp.k_in, lp.k_out, d_out, as_stream(stream)));
+  BMLP_LAUNCH(launch_read_h(ctx->state + lp.off_h, lp.ld_h, lp.h_ps, ctx->plan.bound, lp.k_in, lp.k_out, d_out,
+                            as_stream(stream)));
   return BMLP_OK;
 }
 

@@ -17,10 +17,18 @@ enum : uint32_t {
   kStreamFine = 4,      // reinforcement: low 24 bits of the 32-bit draw
 };
 
+// Bit planes of H: u = (h + B) / 2 lies in [0, B], B odd.
+__host__ __device__ inline int h_planes(int bound) {
+  int m = 1;
+  while ((1 << m) <= bound) ++m;
+  return m;
+}
+
 struct LayerPlan {
   int k_in, k_out, gamma, groups;
   int words_in, words_out;   // uint64 words per bit row of a_{l-1} / a_l
-  int ld_h;                  // bytes per H row, multiple of 64
+  int ld_h;                  // bytes per H row: h_planes planes of h_ps words
+  int h_ps;                  // 32-bit words per plane of an H row, multiple of 16
   int robust_thr;            // ceil(r K_l)
   int ldq_in, ldq_out;       // bytes per fp4 row of K_{l-1} / K_l elements
   size_t off_h, off_w, off_p, off_wq, off_pq;     // state
@@ -50,9 +58,10 @@ hipError_t launch_pack(const int8_t *x, int n, int K, uint64_t *bits, hipStream_
 
 // H_l and W_l of one layer from Philox stream 1 (init) or W_l from the H_l in
 // place (attach); P_l from stream 2.
-hipError_t launch_read_h(const uint8_t *H, int ld_h, int k_in, int k_out, int8_t *out, hipStream_t s);
-hipError_t launch_init_h(uint8_t *H, int ld_h, uint64_t *W, int words_in, int k_in, int k_out,
-                         uint64_t seed, int layer, bool from_h, hipStream_t s);
+hipError_t launch_read_h(const uint8_t *H, int ld_h, int h_ps, int bound, int k_in, int k_out,
+                         int8_t *out, hipStream_t s);
+hipError_t launch_init_h(uint8_t *H, int ld_h, int h_ps, int bound, uint64_t *W, int words_in, int k_in,
+                         int k_out, uint64_t seed, int layer, bool from_h, hipStream_t s);
 hipError_t launch_init_p(uint64_t *P, int words_out, int k_out, int c, uint64_t seed, int layer,
                          hipStream_t s);
 
@@ -158,7 +167,7 @@ struct UpdLayer {
   const uint8_t *upd;      // [n]: only patterns in M_l are used
   const uint64_t *P;
   int32_t *stats;          // this layer's [4]; reads [1] (|M|), adds [2] and [3]
-  int ld_h, nw32, words_out, k_in, groups, gamma;
+  int ld_h, h_ps, nw32, words_out, k_in, groups, gamma;
   int chunks, block0;      // filled by launch_update
   uint32_t t_hi, t_lo;     // T_l >> 24 (0..256) and T_l & 0xFFFFFF
   uint32_t ctr1;           // layer - 1

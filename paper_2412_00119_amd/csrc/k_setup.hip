@@ -27,40 +27,39 @@ __device__ __forceinline__ bool stream_bit(uint64_t j, uint64_t seed, int layer,
   return (pick_word(v, b >> 5) >> (b & 31)) & 1u;
 }
 
-// Grid: (ceil(ld_h / 256), k_out).  Thread = one column of one H row; each
-// wave covers 64 aligned columns, i.e. two 32-column groups of the bit-sliced
-// H (word p of a group = bit p of its 32 int8 values), and ballots both the
-// planes and the W word.  from_h: H is kept and only W = sign(H) is derived
-// (from the sign plane).
-__global__ __launch_bounds__(256) void init_h_kernel(uint8_t *__restrict__ H, int ld_h,
+// Grid: (h_ps * 32 / 256, k_out).  Thread = one column of one H row (h_ps
+// words per plane cover 32 * h_ps >= k_in columns, a multiple of 512, so
+// waves stay whole).  H holds u = (h + B) / 2 in M = bits(B) planes: word
+// p * h_ps + g of a row has bit p of u for the 32 columns of group g; a wave
+// (two groups) ballots each plane and the W word.  Padding columns hold 0.
+// from_h: H is kept and only W = sign(H), i.e. u >= (B + 1) / 2, is derived.
+__global__ __launch_bounds__(256) void init_h_kernel(uint8_t *__restrict__ H, int ld_h, int h_ps, int B,
                                                      uint64_t *__restrict__ W, int words_in,
                                                      int k_in, int k_out, uint64_t seed, int layer,
                                                      int from_h) {
   const int k = blockIdx.y;
   const int i = blockIdx.x * 256 + threadIdx.x;
-  if (k >= k_out || i >= ld_h) return;    // ld_h is a multiple of 64: waves stay whole
+  if (k >= k_out || i >= h_ps * 32) return;
   const int lane = threadIdx.x & 63;
-  uint8_t *grp = H + (size_t)k * ld_h + (size_t)(i >> 5) * 32;   // this column's group
+  const int M = h_planes(B);
+  uint32_t *row = reinterpret_cast<uint32_t *>(H + (size_t)k * ld_h);
+  const int g = i >> 5;
   bool pos;
   if (from_h) {
-    const uint32_t sign = reinterpret_cast<const uint32_t *>(grp)[7];
-    pos = i < k_in && !((sign >> (i & 31)) & 1u);
+    int u = 0;
+    for (int q = 0; q < M; ++q) u |= (int)((row[(size_t)q * h_ps + g] >> (i & 31)) & 1u) << q;
+    pos = i < k_in && u >= (B + 1) / 2;
   } else {
-    int h = 0;   // padding columns hold 0
+    int u = 0;   // padding columns
+    pos = false;
     if (i < k_in) {
       const uint64_t j = (uint64_t)k * (uint64_t)k_in + (uint64_t)i;
-      h = stream_bit(j, seed, layer, kStreamHInit) ? 1 : -1;
+      pos = stream_bit(j, seed, layer, kStreamHInit);
+      u = pos ? (B + 1) / 2 : (B - 1) / 2;   // h = +1 or -1
     }
-    pos = h > 0;
-    uint32_t planes[8];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const uint64_t b = __ballot((h >> q) & 1);
-      planes[q] = (uint32_t)(b >> (lane & 32));
-    }
-    if ((lane & 31) == 0) {
-      reinterpret_cast<uint4 *>(grp)[0] = make_uint4(planes[0], planes[1], planes[2], planes[3]);
-      reinterpret_cast<uint4 *>(grp)[1] = make_uint4(planes[4], planes[5], planes[6], planes[7]);
+    for (int q = 0; q < M; ++q) {
+      const uint64_t b = __ballot((u >> q) & 1);
+      if ((lane & 31) == 0) row[(size_t)q * h_ps + g] = (uint32_t)(b >> (lane & 32));
     }
   }
   const uint64_t m = __ballot(pos);
@@ -68,17 +67,17 @@ __global__ __launch_bounds__(256) void init_h_kernel(uint8_t *__restrict__ H, in
   if (lane == 0 && w < words_in) W[(size_t)k * words_in + w] = m;
 }
 
-// bit-sliced H [k_out][ld_h bytes] -> int8 [k_out][k_in]; one thread per value
-__global__ __launch_bounds__(256) void read_h_kernel(const uint8_t *__restrict__ H, int ld_h, int k_in,
-                                                     int k_out, int8_t *__restrict__ out) {
+// H planes [k_out][ld_h bytes] -> int8 h = 2u - B [k_out][k_in]; one thread per value
+__global__ __launch_bounds__(256) void read_h_kernel(const uint8_t *__restrict__ H, int ld_h, int h_ps, int B,
+                                                     int k_in, int k_out, int8_t *__restrict__ out) {
   const int k = blockIdx.y;
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (k >= k_out || i >= k_in) return;
-  const uint32_t *grp = reinterpret_cast<const uint32_t *>(H + (size_t)k * ld_h + (size_t)(i >> 5) * 32);
-  uint32_t v = 0u;
-#pragma unroll
-  for (int q = 0; q < 8; ++q) v |= ((grp[q] >> (i & 31)) & 1u) << q;
-  out[(size_t)k * k_in + i] = (int8_t)(uint8_t)v;
+  const int M = h_planes(B);
+  const uint32_t *row = reinterpret_cast<const uint32_t *>(H + (size_t)k * ld_h);
+  int u = 0;
+  for (int q = 0; q < M; ++q) u |= (int)((row[(size_t)q * h_ps + (i >> 5)] >> (i & 31)) & 1u) << q;
+  out[(size_t)k * k_in + i] = (int8_t)(2 * u - B);
 }
 
 // Grid: (ceil(words_out / 4), c).  One wave per 64 classifier entries.
@@ -121,17 +120,18 @@ hipError_t launch_pack(const int8_t *x, int n, int K, uint64_t *bits, hipStream_
   return hipGetLastError();
 }
 
-hipError_t launch_init_h(uint8_t *H, int ld_h, uint64_t *W, int words_in, int k_in, int k_out,
-                         uint64_t seed, int layer, bool from_h, hipStream_t s) {
-  hipLaunchKernelGGL(init_h_kernel, dim3(cdiv(ld_h, 256), k_out), dim3(256), 0, s, H, ld_h, W,
+hipError_t launch_init_h(uint8_t *H, int ld_h, int h_ps, int bound, uint64_t *W, int words_in, int k_in,
+                         int k_out, uint64_t seed, int layer, bool from_h, hipStream_t s) {
+  hipLaunchKernelGGL(init_h_kernel, dim3(h_ps * 32 / 256, k_out), dim3(256), 0, s, H, ld_h, h_ps, bound, W,
                      words_in, k_in, k_out, seed, layer, from_h ? 1 : 0);
   return hipGetLastError();
 }
 
-hipError_t launch_read_h(const uint8_t *H, int ld_h, int k_in, int k_out, int8_t *out, hipStream_t s) {
+hipError_t launch_read_h(const uint8_t *H, int ld_h, int h_ps, int bound, int k_in, int k_out,
+                         int8_t *out, hipStream_t s) {
   if (k_in <= 0 || k_out <= 0) return hipSuccess;
-  hipLaunchKernelGGL(read_h_kernel, dim3(cdiv(k_in, 256), k_out), dim3(256), 0, s, H, ld_h, k_in, k_out,
-                     out);
+  hipLaunchKernelGGL(read_h_kernel, dim3(cdiv(k_in, 256), k_out), dim3(256), 0, s, H, ld_h, h_ps, bound, k_in,
+                     k_out, out);
   return hipGetLastError();
 }
 

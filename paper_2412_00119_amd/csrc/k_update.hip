@@ -9,21 +9,23 @@
 // 2 sign(h), -B, B); finally W = sign(H) is written as bits and as fp4.  A
 // layer whose M_l is empty is left untouched.
 //
-// H is stored bit-sliced (see bmlp.h): each 32-column group of a row is eight
-// words, word p holding bit p of the 32 two's-complement int8 values.  A lane
-// owns one group, so every step below works on 32 columns with one bitwise
-// operation per bit plane:
+// h is odd and |h| <= B (B odd), so H is stored as u = (h + B) / 2 in
+// [0, B], in M = bits(B) planes (see bmlp.h): plane p of a row holds bit p of
+// u for every column, one 32-bit word per 32-column group.  A lane owns one
+// group, so every step below works on 32 columns with one bitwise operation
+// per bit plane:
 //   * the count cnt_i of +1 contributions (x = a-word XOR [rho = -1]) of the
 //     S selectors of the row is accumulated bit-sliced (plane p = bit p of
 //     the 32 counters) with carry-save adder trees, the loads of a row's
 //     a-words issued sixteen at a time;
-//   * h + 4 cnt - 2 S (= h + dH) and the clip to [-B, B] are ripple-carry
-//     additions and comparisons on the planes, wide enough to be exact;
+//   * u + 2 cnt - S (= (h + dH + B) / 2) and the clip to [0, B] are
+//     ripple-carry additions and comparisons on the planes, wide enough to
+//     be exact;
 //   * the coarse reinforcement bytes arrive as bit planes (one Philox word
 //     per plane), so "u8 < T >> 24" is an 8-step bit-sliced comparison; the
 //     fine 24 bits are drawn only where u8 == T >> 24;
-//   * h <- h + 2 sign(h) on the fired columns is one more planar addition,
-//     and W = sign(H) is the complement of the sign plane.
+//   * h <- h + 2 sign(h) is u <- u +- 1 on the fired columns, one more planar
+//     addition, and W = sign(H) is u >= (B + 1) / 2.
 //
 // Work-group: (layer, group g), 16 waves.  The group's selections U_l (each
 // pattern in M_l with a wrong perceptron in the group) are bucketed by
@@ -209,45 +211,57 @@ __device__ __forceinline__ uint32_t sign_of_sum(const uint32_t (&x)[NB], uint32_
   return x[NB - 1] ^ kb ^ carry;
 }
 
-// h <- clip(h + 4 cnt - 2 S, -B, B) on the 8 planes of h, computed in NB-bit
-// two's complement.  NB must hold 4 S, and z - (B + 1) and z + B for
-// z = h + 4 cnt - 2 S: 10 bits for S <= 63, 11 for S <= 255, 18 for S <=
-// 16383 (|h|, B <= 127).
-template <int NB>
-__device__ __forceinline__ void cp_apply(uint32_t (&h)[8], const uint32_t (&c)[kPlanes], int S, int B) {
-  // d = 4 cnt - 2 S
+// u <- clip(u + 2 cnt - S, 0, B) on the M planes of u, computed in NB-bit
+// two's complement.  NB must hold z = u + 2 cnt - S, in [-S, B + S], and
+// z - (B + 1): 9 bits for S <= 63, 10 for S <= 255, 17 for S <= 16384
+// (B <= 127).
+template <int M, int NB>
+__device__ __forceinline__ void cp_apply(uint32_t (&u)[M], const uint32_t (&c)[kPlanes], int S, int B) {
+  // z = 2 cnt - S
   uint32_t z[NB];
 #pragma unroll
-  for (int p = 0; p < NB; ++p) z[p] = (p >= 2 && p - 2 < kPlanes) ? c[p - 2] : 0u;
-  add_const<NB>(z, (uint32_t)(-2 * S));
-  // z = h + d, h sign-extended
+  for (int p = 0; p < NB; ++p) z[p] = (p >= 1 && p - 1 < kPlanes) ? c[p - 1] : 0u;
+  add_const<NB>(z, (uint32_t)(-S));
+  // z += u
   uint32_t carry = 0u;
 #pragma unroll
   for (int p = 0; p < NB; ++p) {
-    const uint32_t hp = h[p < 8 ? p : 7];
-    const uint32_t s = z[p] ^ hp ^ carry;
-    carry = maj(z[p], hp, carry);
-    z[p] = s;
+    const uint32_t up = p < M ? u[p] : 0u;
+    const uint32_t t = z[p] ^ up ^ carry;
+    carry = maj(z[p], up, carry);
+    z[p] = t;
   }
-  // z > B  <=>  z - (B + 1) >= 0 ;  z < -B  <=>  z + B < 0
+  // z > B  <=>  z - (B + 1) >= 0 ;  z < 0 is the sign plane
   const uint32_t gt = ~sign_of_sum<NB>(z, (uint32_t)(-(B + 1)));
-  const uint32_t lt = sign_of_sum<NB>(z, (uint32_t)B);
+  const uint32_t lt = z[NB - 1];
 #pragma unroll
-  for (int p = 0; p < 8; ++p) {
-    const uint32_t bp = ((B >> p) & 1) ? 0xFFFFFFFFu : 0u;     // plane p of +B
-    const uint32_t nbp = (((-B) >> p) & 1) ? 0xFFFFFFFFu : 0u;  // plane p of -B
-    h[p] = (z[p] & ~(gt | lt)) | (bp & gt) | (nbp & lt);
+  for (int p = 0; p < M; ++p) {
+    const uint32_t bp = ((B >> p) & 1) ? 0xFFFFFFFFu : 0u;   // plane p of B
+    u[p] = (z[p] & ~(gt | lt)) | (bp & gt);
   }
 }
 
-// Lanes where the 8-plane value equals the constant v.
-__device__ __forceinline__ uint32_t equals(const uint32_t (&h)[8], int v) {
+// Lanes where the M-plane value equals the constant v.
+template <int M>
+__device__ __forceinline__ uint32_t equals(const uint32_t (&u)[M], int v) {
   uint32_t e = 0xFFFFFFFFu;
 #pragma unroll
-  for (int p = 0; p < 8; ++p) e &= ((v >> p) & 1) ? h[p] : ~h[p];
+  for (int p = 0; p < M; ++p) e &= ((v >> p) & 1) ? u[p] : ~u[p];
   return e;
 }
 
+// Lanes where the M-plane value is at least the constant k (0 < k <= 2^M):
+// the sign plane of u - k in M + 1 bits is clear.
+template <int M>
+__device__ __forceinline__ uint32_t at_least(const uint32_t (&u)[M], int k) {
+  uint32_t x[M + 1];
+#pragma unroll
+  for (int p = 0; p < M; ++p) x[p] = u[p];
+  x[M] = 0u;
+  return ~sign_of_sum<M + 1>(x, (uint32_t)(-k));
+}
+
+template <int M>
 __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   extern __shared__ int smem[];
   __shared__ int wsum[kWaves];
@@ -343,14 +357,11 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     const int beg = __builtin_amdgcn_readfirstlane(r ? bucket[r - 1] : 0);
     const int S = __builtin_amdgcn_readfirstlane(bucket[r]) - beg;
 
-    uint8_t *hrow = U.H + (size_t)k * U.ld_h + (size_t)cwc * 32;
-    uint32_t h[8];
-    {
-      const uint4 h0 = reinterpret_cast<const uint4 *>(hrow)[0];
-      const uint4 h1 = reinterpret_cast<const uint4 *>(hrow)[1];
-      h[0] = h0.x; h[1] = h0.y; h[2] = h0.z; h[3] = h0.w;
-      h[4] = h1.x; h[5] = h1.y; h[6] = h1.z; h[7] = h1.w;
-    }
+    // plane p of the lane's group: word p * h_ps + cwc of the row
+    uint32_t *urow = reinterpret_cast<uint32_t *>(U.H + (size_t)k * U.ld_h) + cwc;
+    uint32_t u[M];
+#pragma unroll
+    for (int q = 0; q < M; ++q) u[q] = urow[(size_t)q * U.h_ps];
 
     // ---- coarse reinforcement draws: plane p of the 32 bytes is word p of
     // Philox blocks 2 (k ceil(K/32) + group) and the one after (stream 3) ----
@@ -362,19 +373,21 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     if (S > 0) {
       uint32_t c[kPlanes];
       count_row(c, list, beg, S, U.a32, U.nw32, cwc);
-      uint32_t hn[8];
+      uint32_t un[M];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) hn[q] = h[q];
+      for (int q = 0; q < M; ++q) un[q] = u[q];
       if (S <= 63)
-        cp_apply<10>(hn, c, S, B);
+        cp_apply<M, 9>(un, c, S, B);
       else if (S <= 255)
-        cp_apply<11>(hn, c, S, B);
+        cp_apply<M, 10>(un, c, S, B);
       else
-        cp_apply<18>(hn, c, S, B);
-      // padding columns keep h = 0
+        cp_apply<M, 17>(un, c, S, B);
+      // padding columns keep u = 0
 #pragma unroll
-      for (int q = 0; q < 8; ++q) h[q] = (hn[q] & validmask) | (h[q] & ~validmask);
+      for (int q = 0; q < M; ++q) u[q] = (un[q] & validmask) | (u[q] & ~validmask);
     }
+    // sign(h) after the Clipped-Perceptron step; reinforcement keeps it
+    const uint32_t pos = at_least<M>(u, (B + 1) >> 1);
 
     // ---- which weights reinforce: u8 < T >> 24, or u8 == T >> 24 and the
     // fine 24 bits below T & 0xFFFFFF ---------------------------------------------
@@ -413,27 +426,27 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     }
     nreinf += __popc(fire);
 
-    // ---- h <- clip(h + 2 sign(h)) on the fired weights: |h| = B stays ----------
+    // ---- h <- clip(h + 2 sign(h)) on the fired weights, i.e. u <- u + 1 where
+    // h > 0 and u - 1 where h < 0; |h| = B (u = 0 or B) stays -------------------
     {
-      const uint32_t gmask = fire & ~(equals(h, B) | equals(h, -B));
-      const uint32_t neg = gmask & h[7];
-      // add delta = +2 (0000 0010) or -2 (1111 1110) where gmask is set
-      uint32_t carry = h[1] & gmask;
-      h[1] ^= gmask;
+      const uint32_t gmask = fire & ~(equals<M>(u, 0) | equals<M>(u, B));
+      const uint32_t dn = gmask & ~pos;   // delta -1 = all ones
+      uint32_t carry = u[0] & gmask;
+      u[0] ^= gmask;
 #pragma unroll
-      for (int q = 2; q < 8; ++q) {
-        const uint32_t sum = h[q] ^ neg ^ carry;
-        carry = maj(h[q], neg, carry);
-        h[q] = sum;
+      for (int q = 1; q < M; ++q) {
+        const uint32_t sum = u[q] ^ dn ^ carry;
+        carry = maj(u[q], dn, carry);
+        u[q] = sum;
       }
     }
 
     if (!on) continue;   // lanes past the row took part in the uniform steps only
 
-    // ---- store H and W = sign(H) (h is odd, so the sign plane decides) -------
-    const uint32_t wbits = ~h[7] & validmask;
-    reinterpret_cast<uint4 *>(hrow)[0] = make_uint4(h[0], h[1], h[2], h[3]);
-    reinterpret_cast<uint4 *>(hrow)[1] = make_uint4(h[4], h[5], h[6], h[7]);
+    // ---- store H and W = sign(H) ----------------------------------------------
+    const uint32_t wbits = pos & validmask;
+#pragma unroll
+    for (int q = 0; q < M; ++q) urow[(size_t)q * U.h_ps] = u[q];
     U.W32[(size_t)k * U.nw32 + cw] = wbits;
     {
       uint32_t o[4];
@@ -474,7 +487,17 @@ hipError_t launch_update(UpdateBatch &b, hipStream_t s) {
     blocks += u.groups;
     gmax = max(gmax, u.gamma);
   }
-  hipLaunchKernelGGL(update_kernel, dim3(blocks), dim3(kThreads), update_lds_bytes(gmax, b.n), s, b);
+  const dim3 grid(blocks), block(kThreads);
+  const size_t lds = update_lds_bytes(gmax, b.n);
+  switch (h_planes(b.bound)) {
+    case 1: hipLaunchKernelGGL(update_kernel<1>, grid, block, lds, s, b); break;
+    case 2: hipLaunchKernelGGL(update_kernel<2>, grid, block, lds, s, b); break;
+    case 3: hipLaunchKernelGGL(update_kernel<3>, grid, block, lds, s, b); break;
+    case 4: hipLaunchKernelGGL(update_kernel<4>, grid, block, lds, s, b); break;
+    case 5: hipLaunchKernelGGL(update_kernel<5>, grid, block, lds, s, b); break;
+    case 6: hipLaunchKernelGGL(update_kernel<6>, grid, block, lds, s, b); break;
+    default: hipLaunchKernelGGL(update_kernel<7>, grid, block, lds, s, b); break;
+  }
   return hipGetLastError();
 }
 

@@ -67,7 +67,8 @@ def test_layout_is_aligned_and_disjoint():
     spans = []
     for l in (1, 2):
         i = B.bmlp_describe(cfg, l)
-        assert i.ld_h % 64 == 0 and i.ld_h >= i.k_in
+        assert i.h_planes == 7 and i.h_ps % 16 == 0 and 32 * i.h_ps >= i.k_in
+        assert i.ld_h == 4 * i.h_planes * i.h_ps and i.ld_h % 64 == 0
         for off in (i.off_h, i.off_w, i.off_p, i.off_a, i.off_err, i.off_upd, i.off_kstar):
             assert off % 256 == 0
         spans += [(i.off_h, i.off_h + i.k_out * i.ld_h), (i.off_w, i.off_w + i.k_out * i.words_in * 8),
@@ -121,3 +122,12 @@ def test_stats_stride_matches_binding():
     m = re.search(r"#define\s+BMLP_STATS_STRIDE\s+(\d+)", hdr)
     assert m and int(m.group(1)) == B.STATS_STRIDE
     assert B.STATS_STRIDE * 4 % 128 == 0    # a 128-byte line per layer
+
+
+@pytest.mark.parametrize("bound,planes", [(1, 1), (3, 2), (5, 3), (15, 4), (31, 5), (33, 6), (63, 6), (127, 7)])
+def test_h_planes_hold_offset_values(bound, planes):
+    """H stores u = (h + B) / 2 in [0, B]: bits(B) planes, the fewest that hold B."""
+    i = B.bmlp_describe(B.make_config((100, 64), 10, bound, 64), 1)
+    assert i.h_planes == planes
+    assert (1 << planes) > bound >= (1 << (planes - 1))
+    assert i.ld_h == 4 * planes * i.h_ps and i.h_ps == 16
