@@ -24,6 +24,10 @@ __device__ __forceinline__ uint32_t expand8(uint32_t x) {
   return x;
 }
 
+// fp4 nibbles of 8 bit-encoded ±1 values (bit 1 = +1), all valid: the entry
+// for byte x of a 256-word lookup table
+__device__ __forceinline__ uint32_t fp4_word8(uint32_t x) { return 0xAAAAAAAAu ^ (expand8(x & 0xFFu) << 3); }
+
 // fp4 nibbles of 8 bit-encoded ±1 values (bit 1 = +1); columns whose bit in
 // valid is 0 become 0x0
 __device__ __forceinline__ uint32_t fp4_from_bits8(uint32_t bits, uint32_t valid) {

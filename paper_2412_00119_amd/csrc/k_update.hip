@@ -43,6 +43,19 @@ constexpr int kWaves = 16;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kPlanes = 15;   // counts up to 2^15 - 1 >= BMLP_MAX_BATCH
 
+// A wave-uniform word the compiler must treat as unknown and keep in a
+// scalar register: bit-plane constants (0 or ~0) stay 32-bit operands of
+// the bitwise ops instead of being turned into 64-bit lane masks and
+// selects, and values made from it inside the item loop are not hoisted
+// out of it (where they would no longer fit in scalar registers).
+__device__ __forceinline__ uint32_t opaque(uint32_t v) {
+  asm volatile("" : "+s"(v));
+  return v;
+}
+
+// all-ones when bit p of k is set, else 0, as an opaque scalar
+__device__ __forceinline__ uint32_t plane_of(uint32_t k, int p) { return opaque(0u - ((k >> p) & 1u)); }
+
 __device__ __forceinline__ int wave_sum(int v) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
@@ -191,7 +204,7 @@ __device__ __forceinline__ void add_const(uint32_t (&x)[NB], uint32_t k) {
   uint32_t carry = 0u;
 #pragma unroll
   for (int p = 0; p < NB; ++p) {
-    const uint32_t kb = ((k >> p) & 1u) ? 0xFFFFFFFFu : 0u;
+    const uint32_t kb = plane_of(k, p);
     const uint32_t s = x[p] ^ kb ^ carry;
     carry = maj(x[p], kb, carry);
     x[p] = s;
@@ -203,12 +216,8 @@ template <int NB>
 __device__ __forceinline__ uint32_t sign_of_sum(const uint32_t (&x)[NB], uint32_t k) {
   uint32_t carry = 0u;
 #pragma unroll
-  for (int p = 0; p < NB - 1; ++p) {
-    const uint32_t kb = ((k >> p) & 1u) ? 0xFFFFFFFFu : 0u;
-    carry = maj(x[p], kb, carry);
-  }
-  const uint32_t kb = ((k >> (NB - 1)) & 1u) ? 0xFFFFFFFFu : 0u;
-  return x[NB - 1] ^ kb ^ carry;
+  for (int p = 0; p < NB - 1; ++p) carry = maj(x[p], plane_of(k, p), carry);
+  return x[NB - 1] ^ plane_of(k, NB - 1) ^ carry;
 }
 
 // u <- clip(u + 2 cnt - S, 0, B) on the M planes of u, computed in NB-bit
@@ -235,10 +244,7 @@ __device__ __forceinline__ void cp_apply(uint32_t (&u)[M], const uint32_t (&c)[k
   const uint32_t gt = ~sign_of_sum<NB>(z, (uint32_t)(-(B + 1)));
   const uint32_t lt = z[NB - 1];
 #pragma unroll
-  for (int p = 0; p < M; ++p) {
-    const uint32_t bp = ((B >> p) & 1) ? 0xFFFFFFFFu : 0u;   // plane p of B
-    u[p] = (z[p] & ~(gt | lt)) | (bp & gt);
-  }
+  for (int p = 0; p < M; ++p) u[p] = (z[p] & ~(gt | lt)) | (plane_of((uint32_t)B, p) & gt);
 }
 
 // Lanes where the M-plane value equals the constant v.
@@ -246,7 +252,7 @@ template <int M>
 __device__ __forceinline__ uint32_t equals(const uint32_t (&u)[M], int v) {
   uint32_t e = 0xFFFFFFFFu;
 #pragma unroll
-  for (int p = 0; p < M; ++p) e &= ((v >> p) & 1) ? u[p] : ~u[p];
+  for (int p = 0; p < M; ++p) e &= ~(u[p] ^ plane_of((uint32_t)v, p));
   return e;
 }
 
@@ -266,6 +272,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   extern __shared__ int smem[];
   __shared__ int wsum[kWaves];
   __shared__ int s_sel;
+  __shared__ uint32_t s_fp4[256];   // fp4 word of each byte of signs
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -284,6 +291,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
 
   // ---- bucket the selections of group g by perceptron (counting sort) -------
   if (tid == 0) s_sel = 0;
+  for (int i = tid; i < 256; i += kThreads) s_fp4[i] = fp4_word8((uint32_t)i);
   for (int r = tid; r < gamma; r += kThreads) bucket[r] = 0;
   __syncthreads();
   // U_l: the selections of the patterns in M_l
@@ -366,8 +374,14 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     // ---- coarse reinforcement draws: plane p of the 32 bytes is word p of
     // Philox blocks 2 (k ceil(K/32) + group) and the one after (stream 3) ----
     const uint32_t blk = 2u * ((uint32_t)k * (uint32_t)groups_in + (uint32_t)cwc);
-    const U32x4 v0 = philox4x32_10(blk, U.ctr1, p.step, kStreamCoarse, p.key0, p.key1);
-    const U32x4 v1 = philox4x32_10(blk + 1u, U.ctr1, p.step, kStreamCoarse, p.key0, p.key1);
+    // per-item copies of the uniform constants: what is made from them is
+    // made again in each item, in scalar registers, instead of held across
+    // the loop
+    const uint32_t key0 = opaque(p.key0), key1 = opaque(p.key1);
+    const int Bi = (int)opaque((uint32_t)B);
+    const uint32_t thi = opaque(t_hi);
+    const U32x4 v0 = philox4x32_10(blk, U.ctr1, p.step, kStreamCoarse, key0, key1);
+    const U32x4 v1 = philox4x32_10(blk + 1u, U.ctr1, p.step, kStreamCoarse, key0, key1);
 
     // ---- Clipped-Perceptron sum and clip ------------------------------------
     if (S > 0) {
@@ -377,35 +391,32 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
 #pragma unroll
       for (int q = 0; q < M; ++q) un[q] = u[q];
       if (S <= 63)
-        cp_apply<M, 9>(un, c, S, B);
+        cp_apply<M, 9>(un, c, S, Bi);
       else if (S <= 255)
-        cp_apply<M, 10>(un, c, S, B);
+        cp_apply<M, 10>(un, c, S, Bi);
       else
-        cp_apply<M, 17>(un, c, S, B);
+        cp_apply<M, 17>(un, c, S, Bi);
       // padding columns keep u = 0
 #pragma unroll
       for (int q = 0; q < M; ++q) u[q] = (un[q] & validmask) | (u[q] & ~validmask);
     }
     // sign(h) after the Clipped-Perceptron step; reinforcement keeps it
-    const uint32_t pos = at_least<M>(u, (B + 1) >> 1);
+    const uint32_t pos = at_least<M>(u, (Bi + 1) >> 1);
 
     // ---- which weights reinforce: u8 < T >> 24, or u8 == T >> 24 and the
     // fine 24 bits below T & 0xFFFFFF ---------------------------------------------
     uint32_t fire, need;
-    if (t_hi >= 256u) {
+    if (thi >= 256u) {
       fire = 0xFFFFFFFFu;
       need = 0u;
     } else {
       const uint32_t rp[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
       uint32_t lt = 0u, eq = 0xFFFFFFFFu;
 #pragma unroll
-      for (int q = 7; q >= 0; --q) {
-        if ((t_hi >> q) & 1u) {
-          lt |= eq & ~rp[q];
-          eq &= rp[q];
-        } else {
-          eq &= ~rp[q];
-        }
+      for (int q = 7; q >= 0; --q) {   // from the top bit: u8 < t_hi or still equal
+        const uint32_t tb = plane_of(thi, q);
+        lt |= eq & ~rp[q] & tb;
+        eq &= ~(rp[q] ^ tb);
       }
       fire = lt;
       need = eq;
@@ -421,7 +432,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
       const int e = __ffs(need) - 1;
       need &= need - 1u;
       const uint32_t j = j0 + (uint32_t)e;
-      const U32x4 f = philox4x32_10(j >> 2, U.ctr1, p.step, kStreamFine, p.key0, p.key1);
+      const U32x4 f = philox4x32_10(j >> 2, U.ctr1, p.step, kStreamFine, key0, key1);
       if ((pick_word(f, j & 3u) & 0xFFFFFFu) < t_lo) fire |= 1u << e;
     }
     nreinf += __popc(fire);
@@ -429,7 +440,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     // ---- h <- clip(h + 2 sign(h)) on the fired weights, i.e. u <- u + 1 where
     // h > 0 and u - 1 where h < 0; |h| = B (u = 0 or B) stays -------------------
     {
-      const uint32_t gmask = fire & ~(equals<M>(u, 0) | equals<M>(u, B));
+      const uint32_t gmask = fire & ~(equals<M>(u, 0) | equals<M>(u, Bi));
       const uint32_t dn = gmask & ~pos;   // delta -1 = all ones
       uint32_t carry = u[0] & gmask;
       u[0] ^= gmask;
@@ -450,8 +461,13 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     U.W32[(size_t)k * U.nw32 + cw] = wbits;
     {
       uint32_t o[4];
+      if (validmask == 0xFFFFFFFFu) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) o[q] = fp4_from_bits8(wbits >> (8 * q), validmask >> (8 * q));
+        for (int q = 0; q < 4; ++q) o[q] = s_fp4[(wbits >> (8 * q)) & 0xFFu];
+      } else {   // the row's last, partial group
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] = fp4_from_bits8(wbits >> (8 * q), validmask >> (8 * q));
+      }
       *reinterpret_cast<uint4 *>(U.Wq + (size_t)k * U.ldq + cw * 16) = make_uint4(o[0], o[1], o[2], o[3]);
     }
   }
