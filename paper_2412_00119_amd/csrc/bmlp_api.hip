@@ -235,9 +235,9 @@ int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32
     for (int l = 1; l <= p.L; ++l) {
       const LayerPlan &lp = p.layer[l - 1];
       ClsLayer &c = cb.L[cb.nl++];
-      c.A = ctx->ws + lp.off_aq; c.lda = lp.ldq_out;
-      c.P = ctx->state + lp.off_pq; c.ldp = lp.ldq_out;
-      c.ksteps = lp.ldq_out / 64;
+      c.A = reinterpret_cast<const uint64_t *>(ctx->ws + lp.off_a);
+      c.P = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p);
+      c.words = lp.words_out; c.K = lp.k_out;
       c.yhat = yhat_out ? yhat_out + (size_t)(l - 1) * n * p.c : yh_ws + (size_t)(l - 1) * p.max_batch * p.c;
       c.correct = correct ? correct + (l - 1) : nullptr;
       if (cb.nl == kMaxClsLayers || l == p.L) {
@@ -495,9 +495,9 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
     for (int l = 1; l <= p.L; ++l) {
       const LayerPlan &lp = p.layer[l - 1];
       ClsLayer &c = cb.L[cb.nl++];
-      c.A = ctx->ws + lp.off_aq; c.lda = lp.ldq_out;
-      c.P = ctx->state + lp.off_pq; c.ldp = lp.ldq_out;
-      c.ksteps = lp.ldq_out / 64; c.thr = lp.robust_thr;
+      c.A = reinterpret_cast<const uint64_t *>(ctx->ws + lp.off_a);
+      c.P = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p);
+      c.words = lp.words_out; c.K = lp.k_out; c.thr = lp.robust_thr;
       c.yhat = yh + (size_t)(l - 1) * p.max_batch * p.c;
       c.err = ctx->ws + lp.off_err; c.upd = ctx->ws + lp.off_upd;
       c.stats = d_stats + BMLP_STATS_STRIDE * (l - 1);

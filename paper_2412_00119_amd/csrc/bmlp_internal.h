@@ -120,9 +120,9 @@ hipError_t launch_step_prep(const PrepArgs &a, hipStream_t s);
 // kMaxClsLayers layers in one launch (ceil(n / 16) work-groups per layer).
 enum { kClsTrain = 0, kClsYhatOnly = 1, kClsEval = 2 };
 struct ClsLayer {
-  const uint8_t *A; int lda;        // a_l fp4 [n][lda]
-  const uint8_t *P; int ldp;        // P_l fp4 [c][ldp]
-  int ksteps, thr;
+  const uint64_t *A;                // a_l bit rows [n][words]
+  const uint64_t *P;                // P_l bit rows [c][words]
+  int words, K, thr;                // words = ceil(K / 64)
   int32_t *yhat;                    // y_hat int32 [n][c]: output (kClsYhatOnly), or
                                     // scratch when c needs several passes
   uint8_t *err, *upd;               // train

@@ -24,6 +24,28 @@ __device__ __forceinline__ uint32_t expand8(uint32_t x) {
   return x;
 }
 
+// 32 bit-encoded ±1 values (bit 1 = +1) as one fp4 MFMA operand, in a
+// permuted order: nibble t of output word d holds bit 4t + d.  A dot product
+// is unchanged when both operands use it.  Each word is bit 3 of every nibble
+// set to the complement of the bit, and bit 1 set: 0x2 or 0xA.
+__device__ __forceinline__ uint32_t fp4_sign_nibbles(uint32_t x) { return (x & 0x88888888u) ^ 0xAAAAAAAAu; }
+__device__ __forceinline__ uint4 fp4x32_permuted(uint32_t w) {
+  return make_uint4(fp4_sign_nibbles(w << 3), fp4_sign_nibbles(w << 2), fp4_sign_nibbles(w << 1),
+                    fp4_sign_nibbles(w));
+}
+// the nibbles of fp4x32_permuted whose bit in valid is 0 cleared (padding)
+__device__ __forceinline__ uint4 fp4x32_permuted_masked(uint32_t w, uint32_t valid) {
+  uint4 o = fp4x32_permuted(w);
+  uint32_t m[4];
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    uint32_t x = (valid >> d) & 0x11111111u;
+    x |= x << 1;
+    m[d] = x | (x << 2);
+  }
+  return make_uint4(o.x & m[0], o.y & m[1], o.z & m[2], o.w & m[3]);
+}
+
 // fp4 nibbles of 8 bit-encoded ±1 values (bit 1 = +1), all valid: the entry
 // for byte x of a 256-word lookup table
 __device__ __forceinline__ uint32_t fp4_word8(uint32_t x) { return 0xAAAAAAAAu ^ (expand8(x & 0xFFu) << 3); }

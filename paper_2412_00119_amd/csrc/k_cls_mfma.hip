@@ -3,6 +3,13 @@
 // of Eq. 1 and the robustness test that builds M_l).  The layers are
 // independent once every forward is done, so one launch covers them all.
 //
+// a_l and P_l are read as bit rows: every work-group reads all of P_l, and
+// bits are a quarter of the fp4 bytes.  A lane loads one 32-bit word (32
+// elements of a 128-element K step) of its row and expands it in registers
+// to an fp4 operand; the expansion permutes K inside the word, identically
+// for a_l and P_l, which leaves every dot product unchanged.  Elements past
+// K_l become fp4 zeros in the P operand.
+//
 // A work-group owns 16 patterns of one layer and all classes, taken CB
 // blocks of 16 classes per pass (CB is a template parameter sized to the
 // class count).  Its sixteen waves form KG groups along K times 16 / KG
@@ -11,9 +18,10 @@
 // blocks, over K steps kg, kg + KG, ..., with the operands of kU steps
 // loaded together so that one memory latency covers them.  Loads are
 // unconditional with clamped indices: a clamped row only feeds y_hat
-// entries of patterns past n or classes past c, which are never read.  The partial sums are exact
-// integers: each K group stores its int32 partials in LDS and every thread
-// then adds the KG partials of its own y_hat entries, in a fixed order.
+// entries of patterns past n or classes past c, which are never read.  The
+// partial sums are exact integers: each K group stores its int32 partials
+// in LDS and every thread then adds the KG partials of its own y_hat
+// entries, in a fixed order.
 //
 // Then each wave takes one pattern: first argmax (lowest class on ties), the
 // two largest values (tau = top1 - top2, 0 on a tie), err = (pred != y) and
@@ -22,6 +30,7 @@
 #include <limits.h>
 
 #include "bmlp_internal.h"
+#include "fp4.h"
 
 namespace bmlp {
 namespace {
@@ -59,13 +68,22 @@ struct ClsShape {
   static constexpr int PB = CB < 4 ? CB : 4;     // class blocks per wave
   static constexpr int CG = CB / PB;             // wave groups along the classes
   static constexpr int KG = kWaves / CG;         // wave groups along K
-  static constexpr int kU = KG >= 16 ? 2 : 4;    // K steps loaded together
 };
+
+// K is staged through LDS in chunks of kChunk 32-bit words (4096 elements)
+// per row; rows are padded to kStride words (kStride = 4 mod 64), so the
+// lanes of an operand read (16 rows x 4 consecutive words) hit 64 banks.
+constexpr int kChunk = 128, kStride = kChunk + 4;
 
 template <int CB>
 __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
-  constexpr int PB = ClsShape<CB>::PB, KG = ClsShape<CB>::KG, kU = ClsShape<CB>::kU;
-  __shared__ int red[KG][16][CB * 16];   // per K group; red[0] ends with y_hat
+  constexpr int PB = ClsShape<CB>::PB, KG = ClsShape<CB>::KG;
+  constexpr int kRows = 16 + CB * 16;                      // staged rows: 16 patterns, CB*16 classes
+  constexpr int kStage = kRows * kStride;                  // words
+  constexpr int kRed = KG * 16 * CB * 16;                  // words of the partials
+  __shared__ __align__(16) uint32_t lds[kStage > kRed ? kStage : kRed];
+  uint32_t *const sA = lds, *const sP = lds + 16 * kStride;
+  int (*red)[16][CB * 16] = reinterpret_cast<int (*)[16][CB * 16]>(lds);   // per K group; red[0] ends with y_hat
   __shared__ int cnt[3];                 // block totals of err, upd, correct
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -73,44 +91,64 @@ __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
   const int bpl = (p.n + 15) / 16;               // work-groups per layer
   const ClsLayer &Lr = p.L[blockIdx.x / bpl];
   const int m0 = (blockIdx.x % bpl) * 16;
-  const int lr = lane & 15, lk = (lane >> 4) * 16;
+  const int lr = lane & 15, q = lane >> 4;   // row / class, and which 32 of a K step's 128
   const int nblk = (p.c + 15) / 16;
   const bool one_pass = nblk <= CB;
-  const int am = m0 + lr;
-  // 32-bit byte offsets from the layer's base pointers (scalar base +
-  // vector offset addressing; a_l and P_l are far below 4 GiB)
-  const uint32_t aoff = (uint32_t)min(am, p.n - 1) * (uint32_t)Lr.lda + (uint32_t)lk;
-  const int ksteps = Lr.ksteps;
+  const uint32_t *A32 = reinterpret_cast<const uint32_t *>(Lr.A);
+  const uint32_t *P32 = reinterpret_cast<const uint32_t *>(Lr.P);
+  const int w32 = 2 * Lr.words;                  // 32-bit words per row
   if (tid < 3) cnt[tid] = 0;
 
   for (int cb0 = 0; cb0 < nblk; cb0 += CB) {
     const int nb = min(CB, nblk - cb0);
     v4f acc[PB];
-    uint32_t boff[PB];
 #pragma unroll
-    for (int j = 0; j < PB; ++j) {
-      acc[j] = (v4f){0.f, 0.f, 0.f, 0.f};
-      const int cls = (cb0 + cg * PB + j) * 16 + lr;
-      boff[j] = (uint32_t)min(cls, p.c - 1) * (uint32_t)Lr.ldp + (uint32_t)lk;
-    }
-    const bool any = cg * PB < nb;   // wave-uniform: the wave has a class block in range
-    for (int ks0 = kg; any && ks0 < ksteps; ks0 += KG * kU) {
-      uint4 a[kU], b[kU][PB];
+    for (int j = 0; j < PB; ++j) acc[j] = (v4f){0.f, 0.f, 0.f, 0.f};
+    for (int kw0 = 0; kw0 < w32; kw0 += kChunk) {
+      // stage words kw0 .. kw0 + kChunk of the 16 pattern rows and this
+      // pass's class rows, 16 bytes per thread, coalesced along rows; rows
+      // past n or c repeat the last row, words past the row are 0
+      __syncthreads();   // the previous chunk (or y_hat pass) is no longer read
+      constexpr int kLoads = kRows * (kChunk / 4);                      // 16-byte pieces
+      constexpr int kPer = (kLoads + 64 * kWaves - 1) / (64 * kWaves);    // per thread
+      uint4 v[kPer];
 #pragma unroll
-      for (int u = 0; u < kU; ++u) {
-        const int ks = min(ks0 + u * KG, ksteps - 1);
-        a[u] = *reinterpret_cast<const uint4 *>(Lr.A + (aoff + (uint32_t)ks * 64u));
-#pragma unroll
-        for (int j = 0; j < PB; ++j) b[u][j] = *reinterpret_cast<const uint4 *>(Lr.P + (boff[j] + (uint32_t)ks * 64u));
+      for (int i = 0; i < kPer; ++i) {   // all loads in flight before any store
+        const int t = min(tid + i * 64 * kWaves, kLoads - 1);
+        const int row = t / (kChunk / 4), w = kw0 + (t % (kChunk / 4)) * 4;
+        const uint32_t *src = row < 16 ? A32 + (size_t)min(m0 + row, p.n - 1) * w32
+                                       : P32 + (size_t)min(cb0 * 16 + row - 16, p.c - 1) * w32;
+        // rows are whole u64 words (8-byte aligned), and w32 is even
+        uint2 lo = make_uint2(0u, 0u), hi = make_uint2(0u, 0u);
+        if (w < w32) lo = *reinterpret_cast<const uint2 *>(src + w);
+        if (w + 2 < w32) hi = *reinterpret_cast<const uint2 *>(src + w + 2);
+        v[i] = make_uint4(lo.x, lo.y, hi.x, hi.y);
       }
 #pragma unroll
-      for (int u = 0; u < kU; ++u)
-        if (ks0 + u * KG < ksteps) {
+      for (int i = 0; i < kPer; ++i) {
+        const int t = tid + i * 64 * kWaves;
+        if (t < kLoads) *reinterpret_cast<uint4 *>(lds + (t / (kChunk / 4)) * kStride + (t % (kChunk / 4)) * 4) = v[i];
+      }
+      __syncthreads();
+      const int nsteps = min(kChunk, w32 - kw0 + 3) / 4;   // K steps of 4 words in this chunk
+      if (cg * PB < nb) {   // the wave has a class block in range
+        for (int ks = kg; ks < nsteps; ks += KG) {
+          const int wl = 4 * ks + q;   // the lane's word of the step, in the chunk
+          // elements 32 (kw0 + wl) .. +31; those past K are padding (0 in fp4)
+          const int nv = min(max(Lr.K - 32 * (kw0 + wl), 0), 32);
+          const uint32_t valid = nv == 32 ? 0xFFFFFFFFu : ((1u << nv) - 1u);
+          const uint4 av = fp4x32_permuted(sA[lr * kStride + wl]);
 #pragma unroll
           for (int j = 0; j < PB; ++j)
-            if (cg * PB + j < nb) acc[j] = mfma_fp4(a[u], b[u][j], acc[j]);
+            if (cg * PB + j < nb) {
+              const uint32_t bw = sP[((cg * PB + j) * 16 + lr) * kStride + wl];
+              const uint4 bv = valid == 0xFFFFFFFFu ? fp4x32_permuted(bw) : fp4x32_permuted_masked(bw, valid);
+              acc[j] = mfma_fp4(av, bv, acc[j]);
+            }
         }
+      }
     }
+    __syncthreads();   // the staged chunk is no longer read: red reuses it
     // lane holds classes (cb0 + cg*PB + j)*16 + (lane & 15) of patterns
     // 4*(lane >> 4) + e; blocks past nb are never read
 #pragma unroll
