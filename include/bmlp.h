@@ -124,10 +124,10 @@ typedef struct bmlp_config {
  *                                                    bmlp_read_h unpacks it to int8;
  *                    W_l  uint64 [k_out][words_in]   visible weights sign(H_l), bits;
  *                    P_l  uint64 [n_classes][words_out]  fixed classifier, row y is rho^y;
- *                    and, as matrix-core operands, copies of W_l (off_wq, uint8
- *                    [k_out][ldq_in]) and P_l (off_pq, uint8 [n_classes][ldq_out])
- *                    in fp4 e2m1 (+1 = 0x2, -1 = 0xA, padding 0x0; value k in
- *                    nibble k & 1 of byte k >> 1).
+ *                    and, as the matrix-core forward's operand, a copy of W_l
+ *                    (off_wq, uint8 [k_out][ldq_in]) in fp4 e2m1 (+1 = 0x2,
+ *                    -1 = 0xA, padding 0x0; value k in nibble k & 1 of byte
+ *                    k >> 1).
  *   off_a, off_err, off_upd, off_kstar  byte offsets in the workspace of the
  *                    last train step's
  *                    a_l    uint64 [max_batch][words_out]
@@ -146,7 +146,7 @@ typedef struct bmlp_layer_info {
   uint64_t off_h, off_w, off_p;
   uint64_t off_a, off_err, off_upd, off_kstar;
   int32_t ldq_in, ldq_out;
-  uint64_t off_wq, off_pq, off_aq;
+  uint64_t off_wq, off_aq;
   int32_t h_planes, h_ps;
 } bmlp_layer_info;
 

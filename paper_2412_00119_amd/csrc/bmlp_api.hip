@@ -158,8 +158,6 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
     so = align256(so + (size_t)p->c * lp.words_out * 8);
     lp.off_wq = so;
     so = align256(so + (size_t)lp.k_out * lp.ldq_in);
-    lp.off_pq = so;
-    so = align256(so + (size_t)p->c * lp.ldq_out);
   }
   p->state_bytes = so;
   size_t wo = 0;
@@ -297,11 +295,9 @@ int setup(const bmlp_config *cfg, void *d_state, void *d_ws, void *stream, bmlp_
     hipError_t e = launch_init_h(H, lp.ld_h, lp.h_ps, p.bound, W, lp.words_in, lp.k_in, lp.k_out, p.seed, l,
                                  from_h, s);
     if (e == hipSuccess && !from_h) e = launch_init_p(P, lp.words_out, lp.k_out, p.c, p.seed, l, s);
-    // fp4 operand copies of W_l and P_l for the matrix-core path
+    // the fp4 operand copy of W_l for the matrix-core forward
     if (e == hipSuccess)
       e = launch_fp4_rows(W, lp.words_in, lp.k_in, lp.k_out, ctx->state + lp.off_wq, lp.ldq_in, nullptr, 0, s);
-    if (e == hipSuccess)
-      e = launch_fp4_rows(P, lp.words_out, lp.k_out, p.c, ctx->state + lp.off_pq, lp.ldq_out, nullptr, 0, s);
     if (e != hipSuccess) {
       delete ctx;
       return hip_fail(e, "init");
@@ -355,7 +351,6 @@ int bmlp_describe(const bmlp_config *cfg, int32_t l, bmlp_layer_info *info) {
   info->ldq_in = lp.ldq_in;
   info->ldq_out = lp.ldq_out;
   info->off_wq = lp.off_wq;
-  info->off_pq = lp.off_pq;
   info->off_aq = lp.off_aq;
   return BMLP_OK;
 }

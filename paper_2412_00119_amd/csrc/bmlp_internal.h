@@ -31,7 +31,7 @@ struct LayerPlan {
   int h_ps;                  // 32-bit words per plane of an H row, multiple of 16
   int robust_thr;            // ceil(r K_l)
   int ldq_in, ldq_out;       // bytes per fp4 row of K_{l-1} / K_l elements
-  size_t off_h, off_w, off_p, off_wq, off_pq;     // state
+  size_t off_h, off_w, off_p, off_wq;     // state
   size_t off_a, off_err, off_upd, off_kstar, off_aq, off_rho;   // workspace
 };
 
