@@ -3,25 +3,25 @@
 // of Eq. 1 and the robustness test that builds M_l).  The layers are
 // independent once every forward is done, so one launch covers them all.
 //
-// a_l and P_l are read as bit rows: every work-group reads all of P_l, and
-// bits are a quarter of the fp4 bytes.  A lane loads one 32-bit word (32
-// elements of a 128-element K step) of its row and expands it in registers
-// to an fp4 operand; the expansion permutes K inside the word, identically
-// for a_l and P_l, which leaves every dot product unchanged.  Elements past
-// K_l become fp4 zeros in the P operand.
-//
 // A work-group owns 16 patterns of one layer and all classes, taken CB
 // blocks of 16 classes per pass (CB is a template parameter sized to the
-// class count).  Its sixteen waves form KG groups along K times 16 / KG
-// groups along the classes: a wave runs one
-// v_mfma_scale_f32_16x16x128_f8f6f4 per K step for each of its PB class
-// blocks, over K steps kg, kg + KG, ..., with the operands of kU steps
-// loaded together so that one memory latency covers them.  Loads are
-// unconditional with clamped indices: a clamped row only feeds y_hat
-// entries of patterns past n or classes past c, which are never read.  The
-// partial sums are exact integers: each K group stores its int32 partials
-// in LDS and every thread then adds the KG partials of its own y_hat
-// entries, in a fixed order.
+// class count).  a_l and P_l are read as bit rows: chunks of 4096 columns
+// of the 16 pattern rows and the pass's class rows are staged in LDS with
+// coalesced loads (a load that touched 16 rows at once cost 16 cache-line
+// requests, which bound the kernel), rows padded so that operand reads hit
+// 64 banks.  A lane takes one 32-bit word (32 elements of a 128-element K
+// step) of its row and expands it in registers to an fp4 operand; the
+// expansion permutes K inside the word, identically for a_l and P_l, which
+// leaves every dot product unchanged.  Elements past K_l become fp4 zeros in
+// the P operand.  Rows past n or c repeat the last row: they only feed
+// y_hat entries that are never read.
+//
+// The sixteen waves form KG groups along K times 16 / KG groups along the
+// classes: a wave runs one v_mfma_scale_f32_16x16x128_f8f6f4 per K step for
+// each of its PB class blocks, over the chunk's K steps kg, kg + KG, ....
+// The partial sums are exact integers: each K group stores its int32
+// partials in LDS (over the staged chunk) and every thread then adds the KG
+// partials of its own y_hat entries, in a fixed order.
 //
 // Then each wave takes one pattern: first argmax (lowest class on ties), the
 // two largest values (tau = top1 - top2, 0 on a tie), err = (pred != y) and
