@@ -53,13 +53,12 @@ def workload_macs(w, n):
 def update_bytes(w):
     """Algorithmic HBM bytes of one update launch (all layers): H_l read and
     written at bits(B) bits per weight (u = (h + B) / 2 in bit planes), W_l
-    written as bit rows and as fp4 rows."""
+    written as bit rows."""
     planes = max(1, int(w.bound).bit_length())
     tot = 0
     for l in range(1, len(w.widths)):
         k_in, k_out = w.widths[l - 1], w.widths[l]
-        tot += 2 * k_out * 4 * planes * ((k_in + 31) // 32) + k_out * 8 * ((k_in + 63) // 64) \
-            + k_out * 64 * ((k_in + 127) // 128)
+        tot += 2 * k_out * 4 * planes * ((k_in + 31) // 32) + k_out * 8 * ((k_in + 63) // 64)
     return tot
 
 

@@ -110,7 +110,6 @@ typedef struct bmlp_config {
  *                    ceil(k_in / 32), a multiple of 16).
  *   ld_h             bytes per row of H_l: 4 * h_planes * h_ps.
  *   robust_thr       ceil(r * K_l), computed in IEEE double.
- *   ldq_in/out       bytes per fp4 row of K_{l-1} / K_l values (64 per 128 values).
  *   off_h, off_w, off_p  byte offsets in the state buffer of
  *                    H_l  [k_out][ld_h bytes]  hidden weights, perceptron-major
  *                                                    (the transpose of the paper's
@@ -123,11 +122,7 @@ typedef struct bmlp_config {
  *                                                    past k_in hold u = 0.
  *                                                    bmlp_read_h unpacks it to int8;
  *                    W_l  uint64 [k_out][words_in]   visible weights sign(H_l), bits;
- *                    P_l  uint64 [n_classes][words_out]  fixed classifier, row y is rho^y;
- *                    and, as the matrix-core forward's operand, a copy of W_l
- *                    (off_wq, uint8 [k_out][ldq_in]) in fp4 e2m1 (+1 = 0x2,
- *                    -1 = 0xA, padding 0x0; value k in nibble k & 1 of byte
- *                    k >> 1).
+ *                    P_l  uint64 [n_classes][words_out]  fixed classifier, row y is rho^y.
  *   off_a, off_err, off_upd, off_kstar  byte offsets in the workspace of the
  *                    last train step's
  *                    a_l    uint64 [max_batch][words_out]
@@ -138,15 +133,12 @@ typedef struct bmlp_config {
  *                           group (-1 when the group has none), for every
  *                           pattern; U_l (Algorithm 2) is its restriction to
  *                           the patterns with upd_l = 1
- *                    a_l as fp4 (off_aq, uint8 [max_batch][ldq_out]).
  */
 typedef struct bmlp_layer_info {
   int32_t k_in, k_out, gamma, groups;
   int32_t words_in, words_out, ld_h, robust_thr;
   uint64_t off_h, off_w, off_p;
   uint64_t off_a, off_err, off_upd, off_kstar;
-  int32_t ldq_in, ldq_out;
-  uint64_t off_wq, off_aq;
   int32_t h_planes, h_ps;
 } bmlp_layer_info;
 
@@ -178,8 +170,7 @@ int bmlp_init(const bmlp_config *cfg, void *d_state, void *d_workspace, void *st
               bmlp_ctx **out);
 
 /* Like bmlp_init but keeps H_l and P_l already in d_state (a restored
- * checkpoint) and only recomputes what derives from them: W_l = sign(H_l)
- * and the fp4 copies of W_l and P_l. */
+ * checkpoint) and only recomputes what derives from them: W_l = sign(H_l). */
 int bmlp_attach(const bmlp_config *cfg, void *d_state, void *d_workspace, void *stream,
                 bmlp_ctx **out);
 

@@ -60,8 +60,6 @@ class bmlp_layer_info(ctypes.Structure):
                 ("k_in", "k_out", "gamma", "groups", "words_in", "words_out", "ld_h", "robust_thr")] + \
                [(n, ctypes.c_uint64) for n in
                 ("off_h", "off_w", "off_p", "off_a", "off_err", "off_upd", "off_kstar")] + \
-               [(n, ctypes.c_int32) for n in ("ldq_in", "ldq_out")] + \
-               [(n, ctypes.c_uint64) for n in ("off_wq", "off_aq")] + \
                [(n, ctypes.c_int32) for n in ("h_planes", "h_ps")]
 
 
@@ -341,11 +339,6 @@ class BMLP:
         i = self.info[l - 1]
         return self._view(self.state, i.off_p, self.n_classes * i.words_out * 8, self.torch.int64,
                           (self.n_classes, i.words_out))
-
-    def Wq(self, l: int):
-        """W_l as fp4 operand rows, uint8 [K_l][ldq_in]."""
-        i = self.info[l - 1]
-        return self._view(self.state, i.off_wq, i.k_out * i.ldq_in, self.torch.uint8, (i.k_out, i.ldq_in))
 
     def trace(self, l: int, n: int):
         """Last train step's a_l bits, err, upd and kstar of layer l (first n patterns)."""

@@ -145,8 +145,6 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
     lp.words_out = words64(lp.k_out);
     lp.h_ps = (2 * lp.words_in + 15) / 16 * 16;
     lp.ld_h = 4 * h_planes(p->bound) * lp.h_ps;
-    lp.ldq_in = fp4_row_bytes(lp.k_in);
-    lp.ldq_out = fp4_row_bytes(lp.k_out);
     const double thr = ceil(p->r * (double)lp.k_out);
     if (thr > 2147483647.0) return BMLP_EINVAL;
     lp.robust_thr = (int)thr;
@@ -156,8 +154,6 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
     so = align256(so + (size_t)lp.k_out * lp.words_in * 8);
     lp.off_p = so;
     so = align256(so + (size_t)p->c * lp.words_out * 8);
-    lp.off_wq = so;
-    so = align256(so + (size_t)lp.k_out * lp.ldq_in);
   }
   p->state_bytes = so;
   size_t wo = 0;
@@ -171,14 +167,9 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
     wo = align256(wo + (size_t)nb);
     lp.off_kstar = wo;
     wo = align256(wo + (size_t)nb * lp.groups * 2);
-    lp.off_aq = wo;
-    wo = align256(wo + (size_t)nb * lp.ldq_out);
     lp.off_rho = wo;   // rho^{y^mu} rows [max_batch][words_out] for the fused selection
     wo = align256(wo + (size_t)nb * lp.words_out * 8);
   }
-  p->ldq0 = fp4_row_bytes(p->widths[0]);
-  p->off_xq = wo;
-  wo = align256(wo + (size_t)nb * p->ldq0);
   p->ldz = 64 * words64(kmax);
   p->off_z = wo;
   wo = align256(wo + (size_t)nb * p->ldz * 2);
@@ -211,21 +202,17 @@ int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32
   const Plan &p = ctx->plan;
   int32_t *yh_ws = reinterpret_cast<int32_t *>(ctx->ws + p.off_yhat);
   if (use_mfma(p)) {
-    uint8_t *xq = ctx->ws + p.off_xq;
-    BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s,
-               launch_fp4_rows(x, p.layer[0].words_in, p.widths[0], n, xq, p.ldq0, nullptr, 0, s));
-    const uint8_t *aq_prev = xq;
+    const uint64_t *a_prev = x;
     for (int l = 1; l <= p.L; ++l) {
       const LayerPlan &lp = p.layer[l - 1];
       FwdArgs f{};
-      f.A = aq_prev; f.lda = lp.ldq_in;
-      f.B = ctx->state + lp.off_wq; f.ldb = lp.ldq_in;
-      f.M = n; f.N = lp.k_out; f.ksteps = lp.ldq_in / 64;
+      f.A = a_prev; f.lda = lp.words_in;
+      f.B = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_w); f.ldb = lp.words_in;
+      f.M = n; f.N = lp.k_out; f.K = lp.k_in;
       f.abits = reinterpret_cast<uint64_t *>(ctx->ws + lp.off_a); f.words_out = lp.words_out;
-      f.afp4 = ctx->ws + lp.off_aq; f.ld_af = lp.ldq_out;
       f.mode = kFwdPlain;
       BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s, launch_fwd_fp4(f, s));
-      aq_prev = f.afp4;
+      a_prev = f.abits;
     }
     // every layer's local classifier in one launch per kMaxClsLayers layers
     ClsBatch cb{};
@@ -295,9 +282,6 @@ int setup(const bmlp_config *cfg, void *d_state, void *d_ws, void *stream, bmlp_
     hipError_t e = launch_init_h(H, lp.ld_h, lp.h_ps, p.bound, W, lp.words_in, lp.k_in, lp.k_out, p.seed, l,
                                  from_h, s);
     if (e == hipSuccess && !from_h) e = launch_init_p(P, lp.words_out, lp.k_out, p.c, p.seed, l, s);
-    // the fp4 operand copy of W_l for the matrix-core forward
-    if (e == hipSuccess)
-      e = launch_fp4_rows(W, lp.words_in, lp.k_in, lp.k_out, ctx->state + lp.off_wq, lp.ldq_in, nullptr, 0, s);
     if (e != hipSuccess) {
       delete ctx;
       return hip_fail(e, "init");
@@ -348,10 +332,6 @@ int bmlp_describe(const bmlp_config *cfg, int32_t l, bmlp_layer_info *info) {
   info->off_err = lp.off_err;
   info->off_upd = lp.off_upd;
   info->off_kstar = lp.off_kstar;
-  info->ldq_in = lp.ldq_in;
-  info->ldq_out = lp.ldq_out;
-  info->off_wq = lp.off_wq;
-  info->off_aq = lp.off_aq;
   return BMLP_OK;
 }
 
@@ -410,13 +390,11 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
   if (n == 0) return BMLP_OK;
   int16_t *z = reinterpret_cast<int16_t *>(ctx->ws + p.off_z);
   int32_t *yh = reinterpret_cast<int32_t *>(ctx->ws + p.off_yhat);
-  uint8_t *xq = ctx->ws + p.off_xq;
   if (mfma) {
-    // input as fp4 rows, statistics zeroed, and the rho^{y^mu} rows of every
-    // layer whose selection is fused into its forward
+    // statistics zeroed, and the rho^{y^mu} rows of every layer whose
+    // selection is fused into its forward
     PrepArgs pa{};
-    pa.x = d_x; pa.words = p.layer[0].words_in; pa.K = p.widths[0]; pa.n = n;
-    pa.xq = xq; pa.ldq = p.ldq0;
+    pa.n = n;
     pa.zero = d_stats; pa.nzero = BMLP_STATS_STRIDE * p.L;
     pa.y = d_y; pa.c = p.c;
     for (int l = 1; l <= p.L; ++l) {
@@ -427,16 +405,14 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
         q.rho = reinterpret_cast<uint64_t *>(ctx->ws + lp.off_rho);
         q.words_out = lp.words_out;
       }
-      if (pa.nl == kMaxPrepLayers || (l == p.L && (pa.nl > 0 || pa.xq != nullptr))) {
+      if (pa.nl == kMaxPrepLayers || (l == p.L && (pa.nl > 0 || pa.zero != nullptr))) {
         BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s, launch_step_prep(pa, s));
-        pa.xq = nullptr;   // the input and the statistics are done by the first launch
-        pa.zero = nullptr; pa.nzero = 0;
+        pa.zero = nullptr; pa.nzero = 0;   // the statistics are done by the first launch
         pa.nl = 0;
       }
     }
   }
   const uint64_t *a_prev = d_x;
-  const uint8_t *aq_prev = xq;
   for (int l = 1; l <= p.L; ++l) {
     const LayerPlan &lp = p.layer[l - 1];
     const uint64_t *W = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_w);
@@ -457,11 +433,10 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
       const bool fused = lp.gamma == 64;
       // Algorithm 1 lines 8-9, and Algorithm 2's choice when fused
       FwdArgs f{};
-      f.A = aq_prev; f.lda = lp.ldq_in;
-      f.B = ctx->state + lp.off_wq; f.ldb = lp.ldq_in;
-      f.M = n; f.N = lp.k_out; f.ksteps = lp.ldq_in / 64;
+      f.A = a_prev; f.lda = lp.words_in;
+      f.B = W; f.ldb = lp.words_in;
+      f.M = n; f.N = lp.k_out; f.K = lp.k_in;
       f.abits = a; f.words_out = lp.words_out;
-      f.afp4 = ctx->ws + lp.off_aq; f.ld_af = lp.ldq_out;
       f.mode = fused ? kFwdFusedSelect : kFwdWriteZ;
       f.kstar = kstar; f.ldk = p.max_batch;
       f.rho = reinterpret_cast<const uint64_t *>(ctx->ws + lp.off_rho); f.ldr = lp.words_out;
@@ -471,7 +446,6 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
         ls.yhat = nullptr;
         BMLP_TIMED(ctx, BMLP_KERNEL_SELECT, s, launch_loss_select(ls, s));
       }
-      aq_prev = f.afp4;
     } else {
       BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s,
                  launch_fwd_popcount(a_prev, lp.words_in, lp.k_in, W, n, lp.k_out, z, p.ldz, a,
@@ -512,7 +486,6 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
     UpdLayer &u = ub.L[ub.nl++];
     u.H = ctx->state + lp.off_h;
     u.W32 = reinterpret_cast<uint32_t *>(ctx->state + lp.off_w);
-    u.Wq = ctx->state + lp.off_wq; u.ldq = lp.ldq_in;
     u.a32 = reinterpret_cast<const uint32_t *>(l == 1 ? d_x : reinterpret_cast<const uint64_t *>(
                                                                ctx->ws + p.layer[l - 2].off_a));
     u.kstar = reinterpret_cast<const int16_t *>(ctx->ws + lp.off_kstar);

@@ -30,9 +30,8 @@ struct LayerPlan {
   int ld_h;                  // bytes per H row: h_planes planes of h_ps words
   int h_ps;                  // 32-bit words per plane of an H row, multiple of 16
   int robust_thr;            // ceil(r K_l)
-  int ldq_in, ldq_out;       // bytes per fp4 row of K_{l-1} / K_l elements
-  size_t off_h, off_w, off_p, off_wq;     // state
-  size_t off_a, off_err, off_upd, off_kstar, off_aq, off_rho;   // workspace
+  size_t off_h, off_w, off_p;                              // state
+  size_t off_a, off_err, off_upd, off_kstar, off_rho;      // workspace
 };
 
 struct Plan {
@@ -42,8 +41,7 @@ struct Plan {
   int widths[BMLP_MAX_LAYERS + 1];
   LayerPlan layer[BMLP_MAX_LAYERS];   // layer[l-1] describes layer l
   int ldz;                            // int16 elements per row of the z scratch
-  int ldq0;                           // bytes per fp4 row of the input
-  size_t off_z, off_yhat, off_xq;     // shared scratch in the workspace
+  size_t off_z, off_yhat;             // shared scratch in the workspace
   size_t state_bytes, ws_bytes;
 };
 
@@ -79,14 +77,13 @@ hipError_t launch_fwd_popcount(const uint64_t *a_prev, int words_in, int k_in, c
 hipError_t launch_cls_popcount(const uint64_t *a, int words, int k, const uint64_t *P, int n,
                                int c, int32_t *out, int ldo, hipStream_t s);
 
-// Forward on the matrix cores with fp4 operands.
+// Forward on the matrix cores: bit-row operands expanded to fp4 in registers.
 enum { kFwdFusedSelect = 0, kFwdWriteZ = 1, kFwdPlain = 2 };
 struct FwdArgs {
-  const uint8_t *A; int lda;        // a_{l-1} fp4 [M][lda]
-  const uint8_t *B; int ldb;        // W_l fp4 [N][ldb]
-  int M, N, ksteps;                 // ksteps = lda / 64 (>= 1)
+  const uint64_t *A; int lda;       // a_{l-1} bit rows [M][lda words]
+  const uint64_t *B; int ldb;       // W_l bit rows [N][ldb words]
+  int M, N, K;                      // K = K_{l-1} elements per row (lda, ldb >= ceil(K / 64))
   uint64_t *abits; int words_out;   // a_l bits [M][words_out]
-  uint8_t *afp4; int ld_af;         // a_l fp4 [M][ld_af]
   int mode;
   int16_t *kstar; int ldk;          // kFwdFusedSelect (gamma = 64): raw selection [groups][ldk]
   const uint64_t *rho; int ldr;     // kFwdFusedSelect: rho^{y^mu} rows [M][ldr]
@@ -96,20 +93,15 @@ struct FwdArgs {
 };
 hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s);
 
-// bit rows [R][words] of K columns -> fp4 rows [R][ldq]; also zeroes zero[0..nzero)
-hipError_t launch_fp4_rows(const uint64_t *bits, int words, int K, int R, uint8_t *q, int ldq,
-                           int32_t *zero, int nzero, hipStream_t s);
-
-// The start of a matrix-core train step, in one launch: the input as fp4
-// rows, the statistics zeroed, and for each listed layer the rows
-// rho^{y^mu} of P_l for every pattern (for the forward's fused selection).
+// The start of a matrix-core train step, in one launch: the statistics
+// zeroed, and for each listed layer the rows rho^{y^mu} of P_l for every
+// pattern (for the forward's fused selection).
 constexpr int kMaxPrepLayers = 8;
 struct PrepLayer {
   const uint64_t *P; uint64_t *rho; int words_out;   // rho [n][words_out]
 };
 struct PrepArgs {
-  const uint64_t *x; int words, K, n;   // input bit rows [n][words]
-  uint8_t *xq; int ldq;                 // input fp4 rows [n][ldq]; null: skip
+  int n;
   int32_t *zero; int nzero;
   const int32_t *y; int c;
   PrepLayer L[kMaxPrepLayers]; int nl;
@@ -161,7 +153,6 @@ hipError_t launch_eval_count(const int32_t *yhat, int c, const int32_t *y, int n
 struct UpdLayer {
   uint8_t *H;              // bit-sliced [K_l][ld_h bytes]
   uint32_t *W32;
-  uint8_t *Wq; int ldq;    // W_l as fp4 [K_l][ldq]
   const uint32_t *a32;     // a_{l-1} bit rows as 32-bit words [n][nw32]
   const int16_t *kstar;    // [groups][ldk], for every pattern
   const uint8_t *upd;      // [n]: only patterns in M_l are used

@@ -2,19 +2,27 @@
 // a_l = sign(z)), with the layer-level selection of Algorithm 2 fused into
 // the epilogue.
 //
-// Both operands are ±1 matrices stored as fp4 (see fp4.h), so z is computed
-// exactly by v_mfma_scale_f32_32x32x64_f8f6f4 with fp32 accumulation (on
-// gfx950 the 32x32x64 shape runs fp4 at twice the rate of 16x16x128).  A
-// work-group computes a 128 x 128 tile of z (patterns x perceptrons) with
-// four waves of 64 x 64; K is walked in steps of 128 elements through a
-// ring of kStages LDS buffers filled by direct-to-LDS loads
-// (global_load_lds_dwordx4) three steps ahead of the matrix cores, with one
-// barrier per step; operands are read from LDS one step ahead, in between
-// the MFMAs.  Rows past the matrix end are clamped into range: they only
-// feed outputs that are never stored.  The epilogue never writes z to
+// The operands are the bit rows the rest of the step keeps (bit 1 = +1):
+// a_{l-1} (or the input) and W_l.  Each 32-bit word is expanded in registers
+// to an OCP e2m1 (fp4) MFMA operand, +1 -> 0x2 and -1 -> 0xA, in the K order
+// of fp4x32_permuted; both operands use that order, so every dot product is
+// unchanged.  v_mfma_scale_f32_32x32x64_f8f6f4 multiplies ±1 by ±1 exactly
+// and accumulates in fp32, exact for |z| < 2^24 (on gfx950 the 32x32x64
+// shape runs fp4 at twice the rate of 16x16x128).  The expansion is a few
+// bit operations per MFMA, issued between the MFMAs of the same wave.
+//
+// A work-group computes a 128 x 128 tile of z (patterns x perceptrons) with
+// four waves of 64 x 64.  K is walked in steps of 512 elements (64 bytes of
+// each bit row) through a ring of kStages LDS buffers filled by
+// direct-to-LDS loads (global_load_lds, 16 bytes per lane, or 4 where rows
+// are not 16-byte aligned) three steps ahead of the matrix cores, with one
+// barrier per step; a step's operand words are read from LDS one step
+// ahead, in between the MFMAs.  Rows past the matrix end are clamped into
+// range, and so are loads past the end of a row in the last step: they
+// only feed outputs that are never stored, or elements past K, which are
+// made fp4 zeros in the W_l operand.  The epilogue never writes z to
 // memory:
-//   * a_l as bit rows (wave ballots) and as fp4 rows for the next layer and
-//     the classifier;
+//   * a_l as bit rows (wave ballots);
 //   * for gamma = 64, the easiest wrong perceptron of each group: among the
 //     columns k of the group with delta_k = z_k rho^{y}_k < 0, the smallest
 //     |z_k|, lowest k on ties (key = |z| << 8 | k, min-reduced across lanes
@@ -34,14 +42,20 @@ typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 
 constexpr int TM = 128, TN = 128;   // tile of z
-constexpr int KB = 64;              // bytes per row per K step (128 fp4)
+constexpr int KB = 64;              // bytes per row per K step (512 elements)
 constexpr int kStages = 4;          // LDS ring depth (kStages - 1 steps in flight)
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// 16 bytes per lane from global memory to LDS at dst + 16 * lane
-__device__ __forceinline__ void dma16(const void *src, void *dst_wave_base) {
-  __builtin_amdgcn_global_load_lds(src, (lds_void *)dst_wave_base, 16, 0, 0);
+// UNIT (16 or 4) bytes per lane from global memory to LDS at
+// dst + UNIT * lane
+template <int UNIT>
+__device__ __forceinline__ void dma(const void *src, void *dst_wave_base) {
+  static_assert(UNIT == 16 || UNIT == 4, "load size");
+  if constexpr (UNIT == 16)
+    __builtin_amdgcn_global_load_lds(src, (lds_void *)dst_wave_base, 16, 0, 0);
+  else
+    __builtin_amdgcn_global_load_lds(src, (lds_void *)dst_wave_base, 4, 0, 0);
 }
 
 // v_writelane_b32: lane `lane` of the result takes the wave-uniform value
@@ -62,24 +76,28 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0xF70);
 }
 
-// XOR swizzle of the 16-byte chunk index within a 64-byte LDS row.  LDS has
+// XOR swizzle of the 16-byte unit index within a 64-byte LDS row.  LDS has
 // 64 banks of 4 bytes, so a 64-byte row spans a quarter of them, chosen by
 // r & 3.  On gfx950 a ds_read_b128 is served in four passes of 16 lanes:
 // the lanes that agree in bit 5 and in the parity of bits 2..4 (measured
 // with the bank-conflict counter).  The operand reads give lane l row
 // (l & 31) of a 32-row block, so a pass holds four rows per value of r & 3,
-// whose bits 2..3 take four distinct values; XOR-ing the chunk with them
+// whose bits 2..3 take four distinct values; XOR-ing the unit with them
 // puts the pass on 64 distinct banks.
 __device__ __forceinline__ int swz(int r) { return (r >> 2) & 3; }
 
-// lane l: A row / B column (l & 31), K elements 32*(l >> 5) .. +32 of the
-// 64-element step; result element i of lane l is row 8*(i>>2) + 4*(l>>5) + (i&3),
+// lane l: A row / B column (l & 31), half (l >> 5) of the 64-element K
+// block; result element i of lane l is row 8*(i>>2) + 4*(l>>5) + (i&3),
 // column (l & 31)
 __device__ __forceinline__ v16f mfma_fp4(const uint4 &a, const uint4 &b, v16f c) {
   const v8i av = {(int)a.x, (int)a.y, (int)a.z, (int)a.w, 0, 0, 0, 0};
   const v8i bv = {(int)b.x, (int)b.y, (int)b.z, (int)b.w, 0, 0, 0, 0};
   // operand formats 4 = e2m1 for A and B, unit (E8M0 127) block scales
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, c, 4, 4, 0, 127, 0, 127);
+}
+
+__device__ __forceinline__ uint32_t dword(const uint4 &u, int q) {
+  return q == 0 ? u.x : q == 1 ? u.y : q == 2 ? u.z : u.w;
 }
 
 // one reduce-scatter step at lane distance D, the partner given by DPP
@@ -95,6 +113,9 @@ __device__ __forceinline__ void select_step(uint32_t (&v)[32], int lc) {
   }
 }
 
+// UNIT: bytes per lane of the direct-to-LDS loads, 16 when every operand
+// row starts on a 16-byte boundary, else 4
+template <int UNIT>
 __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   // one LDS array per ring slot (A tile, then B tile): every access below
   // names its array, so the compiler can tell a slot being read from the
@@ -104,6 +125,10 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   __shared__ __align__(16) uint8_t s0[kSlot], s1[kSlot], s2[kSlot], s3[kSlot];
   __shared__ uint64_t sP[2][TM];       // rho^{y^mu} bits of the tile's 128 columns, per group
   static_assert(kStages == 4, "one named array per slot");
+  constexpr int kRowsPerDma = 64 * UNIT / KB;     // rows per load instruction: 16 or 4
+  constexpr int kDma = 32 / kRowsPerDma;          // instructions per operand per wave and step
+  constexpr int kIssue = 2 * kDma;                // loads per wave and step
+  static_assert(kIssue * (kStages - 2) < 64, "vmcnt range");
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
@@ -134,23 +159,30 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   const uint64_t prow = p.rho[(size_t)min(pm, p.M - 1) * p.ldr + min(pwg, p.pw_max)];
   __builtin_amdgcn_sched_barrier(0);
 
-  // Loads: a wave moves rows 32*wave .. 32*wave+31 of each operand, 16 rows
-  // (1 KB) per instruction; lane l fills LDS bytes 16*l of the 1 KB, i.e. row
-  // l >> 2, physical chunk l & 3, which holds logical chunk (l & 3) ^ swz(row)
-  // of that row (the XOR swizzle keeps the MFMA operand reads conflict-free).
-  const uint8_t *srcA[2], *srcB[2];
+  // Loads: a wave moves rows 32*wave .. 32*wave+31 of each operand.  Lane l
+  // of instruction h fills LDS bytes UNIT*l of its kRowsPerDma rows: row
+  // r = 32*wave + kRowsPerDma*h + (UNIT*l) / 64, physical 16-byte unit u,
+  // which holds logical unit u ^ swz(r) of that row (the XOR swizzle keeps
+  // the operand reads conflict-free).  A source past the end of its row
+  // (only in the last step) is clamped to the row's last UNIT bytes.
+  const uint8_t *srcA[kDma], *srcB[kDma];
+  int offA[kDma];
+  const int rowbytes_a = 8 * p.lda, rowbytes_b = 8 * p.ldb;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int r = 32 * wave + 16 * h + (lane >> 2);
-    const int c = (lane & 3) ^ swz(r);
-    srcA[h] = p.A + (size_t)min(m0 + r, p.M - 1) * p.lda + c * 16;
-    srcB[h] = p.B + (size_t)min(n0 + r, p.N - 1) * p.ldb + c * 16;
+  for (int h = 0; h < kDma; ++h) {
+    const int pos = UNIT * lane;   // byte in the instruction's rows
+    const int r = 32 * wave + kRowsPerDma * h + pos / KB;
+    const int inrow = pos % KB;
+    offA[h] = 16 * ((inrow / 16) ^ swz(r)) + inrow % 16;
+    srcA[h] = reinterpret_cast<const uint8_t *>(p.A + (size_t)min(m0 + r, p.M - 1) * p.lda);
+    srcB[h] = reinterpret_cast<const uint8_t *>(p.B + (size_t)min(n0 + r, p.N - 1) * p.ldb);
   }
   auto issue = [&](int ks, uint8_t *d) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      dma16(srcA[h] + ks * KB, d + (2 * wave + h) * 1024);
-      dma16(srcB[h] + ks * KB, d + TM * KB + (2 * wave + h) * 1024);
+    for (int h = 0; h < kDma; ++h) {
+      const int o = ks * KB + offA[h];
+      dma<UNIT>(srcA[h] + min(o, rowbytes_a - UNIT), d + (kDma * wave + h) * 64 * UNIT);
+      dma<UNIT>(srcB[h] + min(o, rowbytes_b - UNIT), d + TM * KB + (kDma * wave + h) * 64 * UNIT);
     }
   };
 
@@ -160,7 +192,8 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = (v16f){};
 
-  // operands of one K step: [kh][i] for the two 64-element halves
+  // operand words of one K step: [c][i] for its two 256-element chunks;
+  // lane (r, h) holds elements 256 c + 128 h .. +127 of row r
   struct Ops {
     uint4 a[2][2], b[2][2];
   };
@@ -168,23 +201,52 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   auto read = [&](Ops &o, const uint8_t *t) {
     const uint8_t *tA = t, *tB = t + TM * KB;
 #pragma unroll
-    for (int kh = 0; kh < 2; ++kh) {
-      const int ch = 2 * kh + ahalf;   // 16-byte chunk of the 64-byte K step
+    for (int c = 0; c < 2; ++c) {
+      const int u = 2 * c + ahalf;   // 16-byte unit of the 64-byte row
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         const int ra_ = wm * 64 + i * 32 + arow, rb_ = wn * 64 + i * 32 + arow;
-        o.a[kh][i] = *reinterpret_cast<const uint4 *>(&tA[ra_ * KB + ((ch ^ swz(ra_)) * 16)]);
-        o.b[kh][i] = *reinterpret_cast<const uint4 *>(&tB[rb_ * KB + ((ch ^ swz(rb_)) * 16)]);
+        o.a[c][i] = *reinterpret_cast<const uint4 *>(&tA[ra_ * KB + ((u ^ swz(ra_)) * 16)]);
+        o.b[c][i] = *reinterpret_cast<const uint4 *>(&tB[rb_ * KB + ((u ^ swz(rb_)) * 16)]);
       }
     }
   };
+  // MFMA K block (c, q): dword q of the lane's 16 bytes of chunk c
   auto compute = [&](const Ops &o) {
 #pragma unroll
-    for (int kh = 0; kh < 2; ++kh)
+    for (int c = 0; c < 2; ++c)
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int q = 0; q < 4; ++q) {
+        uint4 ea[2], eb[2];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mfma_fp4(o.a[kh][i], o.b[kh][j], acc[i][j]);
+        for (int i = 0; i < 2; ++i) ea[i] = fp4x32_permuted(dword(o.a[c][i], q));
+#pragma unroll
+        for (int j = 0; j < 2; ++j) eb[j] = fp4x32_permuted(dword(o.b[c][j], q));
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j) acc[i][j] = mfma_fp4(ea[i], eb[j], acc[i][j]);
+      }
+  };
+  // the last step when K is not a multiple of 512: elements past K become
+  // fp4 zeros in the W_l operand
+  auto compute_tail = [&](const Ops &o, int ks) {
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int nv = p.K - (512 * ks + 256 * c + 128 * ahalf + 32 * q);
+        const uint32_t valid = nv >= 32 ? 0xFFFFFFFFu : nv <= 0 ? 0u : ((1u << nv) - 1u);
+        uint4 ea[2], eb[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) ea[i] = fp4x32_permuted(dword(o.a[c][i], q));
+#pragma unroll
+        for (int j = 0; j < 2; ++j) eb[j] = fp4x32_permuted_masked(dword(o.b[c][j], q), valid);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j) acc[i][j] = mfma_fp4(ea[i], eb[j], acc[i][j]);
+      }
   };
 
   // Pipeline of step ks: the loads of step ks+3 are issued into the slot of
@@ -197,23 +259,25 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   // repeat the last step into slots nobody reads.  So the count of loads in
   // flight is the same at every step and the code has no branches for the
   // compiler's wait-count tracking to merge over (a merge makes it wait for
-  // every load before the next LDS read).
-  const int nks = p.ksteps;
-  const int klast = nks - 1;   // nks >= 1
+  // every load before the next LDS read).  A partial last step is computed
+  // after the loop.
+  const int nks = (p.K + 511) / 512;
+  const int nfull = p.K / 512;      // steps with no element past K
+  const int klast = nks - 1;        // nks >= 1
   issue(0, s0);
   issue(min(1, klast), s1);
   issue(min(2, klast), s2);
   __builtin_amdgcn_sched_barrier(0);
   Ops r0, r1;
-  wait_vm<4 * (kStages - 2)>();   // this wave's loads of step 0 are done
-  __builtin_amdgcn_s_barrier();    // every wave's loads of step 0 have landed
+  wait_vm<kIssue * (kStages - 2)>();   // this wave's loads of step 0 are done
+  __builtin_amdgcn_s_barrier();        // every wave's loads of step 0 have landed
   read(r0, s0);
   __builtin_amdgcn_sched_barrier(0);
   // The sched_barrier(0) fences pin the order of the phases; otherwise the
   // scheduler sinks the read-ahead to its use and the LDS latency reappears.
   auto step = [&](int ks, Ops &cur, Ops &nxt, const uint8_t *rs, uint8_t *ds) {
     __builtin_amdgcn_sched_barrier(0);
-    wait_vm<4 * (kStages - 3)>();   // step ks+1 landed; ks+2 may still be in flight
+    wait_vm<kIssue * (kStages - 3)>();   // step ks+1 landed; ks+2 may still be in flight
     // A plain s_barrier: the fence of __syncthreads would also wait for the
     // loads still in flight for later steps.
     __builtin_amdgcn_s_barrier();
@@ -221,7 +285,8 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     __builtin_amdgcn_sched_barrier(0);
     compute(cur);
     read(nxt, rs);   // past the last step this reads a slot nobody uses
-    // one LDS read after each MFMA
+    // one LDS read after each of the first MFMAs (issued before them, the
+    // reads would share the wait-count of the operands being consumed)
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
@@ -231,20 +296,32 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   };
   // step ks reads slot (ks+1) % 4 and refills slot (ks+3) % 4
   int ks = 0;
-  for (; ks + kStages <= nks; ks += kStages) {
+  for (; ks + kStages <= nfull; ks += kStages) {
     step(ks + 0, r0, r1, s1, s3);
     step(ks + 1, r1, r0, s2, s0);
     step(ks + 2, r0, r1, s3, s1);
     step(ks + 3, r1, r0, s0, s2);
   }
-  if (ks < nks) {   // the last nks % 4 steps
+  // the last nfull % 4 full steps; r0 then holds the next step's operands
+  if (ks < nfull) {
     step(ks + 0, r0, r1, s1, s3);
-    if (ks + 1 < nks) step(ks + 1, r1, r0, s2, s0);
-    if (ks + 2 < nks) step(ks + 2, r0, r1, s3, s1);
+    if (ks + 1 < nfull) {
+      step(ks + 1, r1, r0, s2, s0);
+      if (ks + 2 < nfull) {
+        step(ks + 2, r0, r1, s3, s1);
+        r0 = r1;
+      }
+    } else {
+      r0 = r1;
+    }
   }
-  wait_vm<0>();   // the repeated loads of the last steps have landed
+  if (nfull < nks) compute_tail(r0, nfull);
   sP[pw][pr] = pvalid ? prow : 0ull;
-  __syncthreads();
+  // A plain barrier after the LDS writes: a __syncthreads fence would also
+  // wait for the repeated loads of the last steps, which land during the
+  // epilogue instead (and are waited for before the wave ends).
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0) only
+  __builtin_amdgcn_s_barrier();
 
   // ---- epilogue ---------------------------------------------------------------
   // lane holds z for column n0 + wn*64 + j*32 + (lane & 31) and rows
@@ -253,7 +330,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   // a_l = sign(z): the ballot of (i, j, e) holds the signs of 32 columns
   // (half j of the wave's 64) of two rows (lanes 0-31 and 32-63).  Ballot
   // k = 16 (2i + j) + e is moved to lane k, which then writes both rows' 32
-  // bits and their fp4 form: no LDS round trip, four stores per lane.
+  // bits: no LDS round trip, two stores per lane.
   uint32_t blo = 0u, bhi = 0u;
   uint64_t colok[2];
 #pragma unroll
@@ -272,22 +349,13 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   {
     const int i = lane >> 5, j = (lane >> 4) & 1, e = lane & 15;
     const int rl0 = wm * 64 + i * 32 + 8 * (e >> 2) + (e & 3);   // the lanes-0-31 row; +4 for 32-63
-    const int cb = n0 + wn * 64 + j * 32;                          // first of the 32 columns
-    const int nv = min(max(p.N - cb, 0), 32);
-    const uint32_t valid = nv == 32 ? 0xFFFFFFFFu : ((1u << nv) - 1u);
+    const int cw = ((n0 + wn * 64) >> 5) + j;                      // 32-bit word of the 32 columns
     uint32_t *ab32 = reinterpret_cast<uint32_t *>(p.abits);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int m = m0 + rl0 + 4 * h;
-      const uint32_t bits = h ? bhi : blo;
-      if (m < p.M) {
-        // the bit row's 32-bit half (columns past N are 0 in the ballot)
-        if ((cb >> 5) < 2 * p.words_out) ab32[(size_t)m * 2 * p.words_out + (cb >> 5)] = bits;
-        uint32_t o[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] = fp4_from_bits8(bits >> (8 * q), valid >> (8 * q));
-        *reinterpret_cast<uint4 *>(p.afp4 + (size_t)m * p.ld_af + (cb >> 1)) = make_uint4(o[0], o[1], o[2], o[3]);
-      }
+      // columns past N are 0 in the ballot
+      if (m < p.M && cw < 2 * p.words_out) ab32[(size_t)m * 2 * p.words_out + cw] = h ? bhi : blo;
     }
   }
 
@@ -355,53 +423,16 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
           if (m < p.M && col < p.N) p.z[(size_t)m * p.ldz + col] = (int16_t)(int)acc[i][j][e];
         }
   }
+  wait_vm<0>();   // the repeated loads write LDS: they land before the wave ends
 }
 
-// bit rows [R][words] -> fp4 rows [R][ldq]; one thread per 16 output bytes
-// (32 columns, one 32-bit word of bits).  Also zeroes `zero[0..nzero)` (the
-// step statistics).
-__global__ __launch_bounds__(256) void fp4_rows_kernel(const uint64_t *__restrict__ bits, int words,
-                                                       int K, int R, uint8_t *__restrict__ q, int ldq,
-                                                       int32_t *zero, int nzero) {
-  const int per_row = ldq >> 4;   // ldq is a multiple of 64
-  const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (zero != nullptr && t < nzero) zero[t] = 0;
-  if (t >= (long long)R * per_row) return;
-  const int r = (int)(t / per_row), d = (int)(t % per_row);
-  const int c0 = d * 32;                       // first column of these 16 bytes
-  uint32_t b = 0u, valid = 0u;
-  if (c0 < K) {
-    b = reinterpret_cast<const uint32_t *>(bits + (size_t)r * words)[c0 >> 5];
-    const int nv = min(K - c0, 32);
-    valid = nv == 32 ? 0xFFFFFFFFu : ((1u << nv) - 1u);
-  }
-  uint32_t o[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) o[i] = fp4_from_bits8(b >> (8 * i), valid >> (8 * i));
-  reinterpret_cast<uint4 *>(q + (size_t)r * ldq)[d] = make_uint4(o[0], o[1], o[2], o[3]);
-}
-
-// blockIdx.y = 0: input fp4 rows (and the statistics zeroed); 1 + i: the
-// rho rows of layer i of the batch, one thread per 64-bit word.
+// Zeroes the statistics and, for each listed layer, gathers the rows
+// rho^{y^mu} of P_l of the batch, one thread per 64-bit word (blockIdx.y =
+// 0: statistics; 1 + i: layer i).
 __global__ __launch_bounds__(256) void step_prep_kernel(PrepArgs p) {
   const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
   if (blockIdx.y == 0) {
     if (p.zero != nullptr && t < p.nzero) p.zero[t] = 0;
-    if (p.xq == nullptr) return;
-    const int per_row = p.ldq >> 4;
-    if (t >= (long long)p.n * per_row) return;
-    const int r = (int)(t / per_row), d = (int)(t % per_row);
-    const int c0 = d * 32;
-    uint32_t b = 0u, valid = 0u;
-    if (c0 < p.K) {
-      b = reinterpret_cast<const uint32_t *>(p.x + (size_t)r * p.words)[c0 >> 5];
-      const int nv = min(p.K - c0, 32);
-      valid = nv == 32 ? 0xFFFFFFFFu : ((1u << nv) - 1u);
-    }
-    uint32_t o[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) o[i] = fp4_from_bits8(b >> (8 * i), valid >> (8 * i));
-    reinterpret_cast<uint4 *>(p.xq + (size_t)r * p.ldq)[d] = make_uint4(o[0], o[1], o[2], o[3]);
     return;
   }
   const PrepLayer &L = p.L[blockIdx.y - 1];
@@ -415,38 +446,34 @@ __global__ __launch_bounds__(256) void step_prep_kernel(PrepArgs p) {
 
 hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
+  if (a.K < 1 || a.N < 1 || a.lda < (a.K + 63) / 64 || a.ldb < (a.K + 63) / 64) return hipErrorInvalidValue;
   a.nt_m = (a.M + TM - 1) / TM;
   a.nt_n = (a.N + TN - 1) / TN;
   a.xcd_remap = (a.nt_n % 8 == 0) ? 1 : 0;
   if (a.mode == kFwdFusedSelect) {
     a.pw_max = a.words_out - 1;
   } else {   // the kernel's rho load reads A instead (always valid)
-    a.rho = reinterpret_cast<const uint64_t *>(a.A);
+    a.rho = a.A;
     a.ldr = 0;
     a.pw_max = 0;
   }
-  hipLaunchKernelGGL(fwd_fp4_kernel, dim3(a.nt_m * a.nt_n), dim3(256), 0, s, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_fp4_rows(const uint64_t *bits, int words, int K, int R, uint8_t *q, int ldq,
-                           int32_t *zero, int nzero, hipStream_t s) {
-  const long long total = (long long)R * (ldq >> 4);
-  const long long need = total > nzero ? total : nzero;
-  if (need <= 0) return hipSuccess;
-  hipLaunchKernelGGL(fp4_rows_kernel, dim3((unsigned)((need + 255) / 256)), dim3(256), 0, s, bits, words,
-                     K, R, q, ldq, zero, nzero);
+  // rows start on 16-byte boundaries when the bases are 16-byte aligned and
+  // the strides are even numbers of words
+  const bool aligned = a.lda % 2 == 0 && a.ldb % 2 == 0 && (reinterpret_cast<uintptr_t>(a.A) & 15) == 0 &&
+                       (reinterpret_cast<uintptr_t>(a.B) & 15) == 0;
+  if (aligned)
+    hipLaunchKernelGGL(fwd_fp4_kernel<16>, dim3(a.nt_m * a.nt_n), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(fwd_fp4_kernel<4>, dim3(a.nt_m * a.nt_n), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_step_prep(const PrepArgs &a, hipStream_t s) {
   long long need = a.nzero;
-  if (a.xq != nullptr) need = std::max(need, (long long)a.n * (a.ldq >> 4));
   for (int i = 0; i < a.nl; ++i) need = std::max(need, (long long)a.n * a.L[i].words_out);
   if (need <= 0) return hipSuccess;
   hipLaunchKernelGGL(step_prep_kernel, dim3((unsigned)((need + 255) / 256), 1 + a.nl), dim3(256), 0, s, a);
   return hipGetLastError();
 }
-
 
 }  // namespace bmlp

@@ -6,7 +6,7 @@
 //   dH[k][i] = 2 * sum over patterns mu that selected k of rho^{y^mu}_k a^mu_i,
 // then h <- clip(h + dH, -B, B); then every hidden weight whose 32-bit
 // Philox draw is below T_l moves one step away from zero, h <- clip(h +
-// 2 sign(h), -B, B); finally W = sign(H) is written as bits and as fp4.  A
+// 2 sign(h), -B, B); finally W = sign(H) is written as bits.  A
 // layer whose M_l is empty is left untouched.
 //
 // h is odd and |h| <= B (B odd), so H is stored as u = (h + B) / 2 in
@@ -33,7 +33,6 @@
 // 2048-column chunk) items, lane l owning 32-column group chunk * 64 + l.  No
 // two work-groups write the same bytes of H or W.
 #include "bmlp_internal.h"
-#include "fp4.h"
 #include "philox.h"
 
 namespace bmlp {
@@ -272,7 +271,6 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   extern __shared__ int smem[];
   __shared__ int wsum[kWaves];
   __shared__ int s_sel;
-  __shared__ uint32_t s_fp4[256];   // fp4 word of each byte of signs
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -291,7 +289,6 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
 
   // ---- bucket the selections of group g by perceptron (counting sort) -------
   if (tid == 0) s_sel = 0;
-  for (int i = tid; i < 256; i += kThreads) s_fp4[i] = fp4_word8((uint32_t)i);
   for (int r = tid; r < gamma; r += kThreads) bucket[r] = 0;
   __syncthreads();
   // U_l: the selections of the patterns in M_l
@@ -459,17 +456,6 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
 #pragma unroll
     for (int q = 0; q < M; ++q) urow[(size_t)q * U.h_ps] = u[q];
     U.W32[(size_t)k * U.nw32 + cw] = wbits;
-    {
-      uint32_t o[4];
-      if (validmask == 0xFFFFFFFFu) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] = s_fp4[(wbits >> (8 * q)) & 0xFFu];
-      } else {   // the row's last, partial group
-#pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] = fp4_from_bits8(wbits >> (8 * q), validmask >> (8 * q));
-      }
-      *reinterpret_cast<uint4 *>(U.Wq + (size_t)k * U.ldq + cw * 16) = make_uint4(o[0], o[1], o[2], o[3]);
-    }
   }
 
   nreinf = wave_sum(nreinf);

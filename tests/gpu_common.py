@@ -28,15 +28,6 @@ def unpack(bits_t, K: int) -> np.ndarray:
     return np.where(b[:, :K] == 1, 1, -1).astype(np.int8)
 
 
-def fp4_np(pm1: np.ndarray, row_bytes: int) -> np.ndarray:
-    """int8 ±1 [n][K] -> fp4 e2m1 rows (+1 = 0x2, -1 = 0xA, padding 0), value k in
-    nibble k & 1 of byte k >> 1."""
-    n, K = pm1.shape
-    nib = np.zeros((n, row_bytes * 2), dtype=np.uint8)
-    nib[:, :K] = np.where(pm1 > 0, 0x2, 0xA)
-    return (nib[:, 0::2] | (nib[:, 1::2] << 4)).astype(np.uint8)
-
-
 def pack_np(pm1: np.ndarray, words: int) -> np.ndarray:
     """int8 ±1 [n][K] -> uint64 [n][words] with zero tail bits (numpy route)."""
     n, K = pm1.shape
@@ -76,8 +67,6 @@ class Pair:
             Pg = self.gpu.P(l).cpu().numpy().view(np.uint64)
             np.testing.assert_array_equal(Pg, pack_np(self.ora.P[l - 1], Pg.shape[1]),
                                           err_msg=f"{tag} P layer {l}")
-            Wq = self.gpu.Wq(l).cpu().numpy()
-            np.testing.assert_array_equal(Wq, fp4_np(self.ora.W(l), Wq.shape[1]), err_msg=f"{tag} Wq layer {l}")
 
     def step(self, x, y, t, p_r, check_state=True, tag=""):
         torch = self.torch
