@@ -167,8 +167,6 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
     wo = align256(wo + (size_t)nb);
     lp.off_kstar = wo;
     wo = align256(wo + (size_t)nb * lp.groups * 2);
-    lp.off_rho = wo;   // rho^{y^mu} rows [max_batch][words_out] for the fused selection
-    wo = align256(wo + (size_t)nb * lp.words_out * 8);
   }
   p->ldz = 64 * words64(kmax);
   p->off_z = wo;
@@ -390,28 +388,6 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
   if (n == 0) return BMLP_OK;
   int16_t *z = reinterpret_cast<int16_t *>(ctx->ws + p.off_z);
   int32_t *yh = reinterpret_cast<int32_t *>(ctx->ws + p.off_yhat);
-  if (mfma) {
-    // statistics zeroed, and the rho^{y^mu} rows of every layer whose
-    // selection is fused into its forward
-    PrepArgs pa{};
-    pa.n = n;
-    pa.zero = d_stats; pa.nzero = BMLP_STATS_STRIDE * p.L;
-    pa.y = d_y; pa.c = p.c;
-    for (int l = 1; l <= p.L; ++l) {
-      const LayerPlan &lp = p.layer[l - 1];
-      if (lp.gamma == 64) {
-        PrepLayer &q = pa.L[pa.nl++];
-        q.P = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p);
-        q.rho = reinterpret_cast<uint64_t *>(ctx->ws + lp.off_rho);
-        q.words_out = lp.words_out;
-      }
-      if (pa.nl == kMaxPrepLayers || (l == p.L && (pa.nl > 0 || pa.zero != nullptr))) {
-        BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s, launch_step_prep(pa, s));
-        pa.zero = nullptr; pa.nzero = 0;   // the statistics are done by the first launch
-        pa.nl = 0;
-      }
-    }
-  }
   const uint64_t *a_prev = d_x;
   for (int l = 1; l <= p.L; ++l) {
     const LayerPlan &lp = p.layer[l - 1];
@@ -439,8 +415,11 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
       f.abits = a; f.words_out = lp.words_out;
       f.mode = fused ? kFwdFusedSelect : kFwdWriteZ;
       f.kstar = kstar; f.ldk = p.max_batch;
-      f.rho = reinterpret_cast<const uint64_t *>(ctx->ws + lp.off_rho); f.ldr = lp.words_out;
+      f.y = d_y; f.c = p.c; f.P = P; f.ldp = lp.words_out;
       f.z = z; f.ldz = p.ldz;
+      if (l == 1) {   // the step statistics start at zero
+        f.zero = d_stats; f.nzero = BMLP_STATS_STRIDE * p.L;
+      }
       BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s, launch_fwd_fp4(f, s));
       if (!fused) {   // Algorithm 2 from the stored z, before the next layer reuses it
         ls.yhat = nullptr;

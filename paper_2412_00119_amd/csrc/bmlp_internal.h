@@ -31,7 +31,7 @@ struct LayerPlan {
   int h_ps;                  // 32-bit words per plane of an H row, multiple of 16
   int robust_thr;            // ceil(r K_l)
   size_t off_h, off_w, off_p;                              // state
-  size_t off_a, off_err, off_upd, off_kstar, off_rho;      // workspace
+  size_t off_a, off_err, off_upd, off_kstar;               // workspace
 };
 
 struct Plan {
@@ -86,27 +86,14 @@ struct FwdArgs {
   uint64_t *abits; int words_out;   // a_l bits [M][words_out]
   int mode;
   int16_t *kstar; int ldk;          // kFwdFusedSelect (gamma = 64): raw selection [groups][ldk]
-  const uint64_t *rho; int ldr;     // kFwdFusedSelect: rho^{y^mu} rows [M][ldr]
+  const int32_t *y; int c;          // kFwdFusedSelect: labels [M] and class count
+  const uint64_t *P; int ldp;       // kFwdFusedSelect: P_l rows [c][ldp], rho^{y^mu} = P_l[y^mu]
   int16_t *z; int ldz;              // kFwdWriteZ
+  int32_t *zero; int nzero;         // if set: zeroed by the first work-group (step statistics)
   int nt_m, nt_n, xcd_remap;        // set by the launcher
-  int pw_max;                       // set by the launcher: last word of a rho row
+  int pw_max, ystride;              // set by the launcher: last word of a P row; label stride
 };
 hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s);
-
-// The start of a matrix-core train step, in one launch: the statistics
-// zeroed, and for each listed layer the rows rho^{y^mu} of P_l for every
-// pattern (for the forward's fused selection).
-constexpr int kMaxPrepLayers = 8;
-struct PrepLayer {
-  const uint64_t *P; uint64_t *rho; int words_out;   // rho [n][words_out]
-};
-struct PrepArgs {
-  int n;
-  int32_t *zero; int nzero;
-  const int32_t *y; int c;
-  PrepLayer L[kMaxPrepLayers]; int nl;
-};
-hipError_t launch_step_prep(const PrepArgs &a, hipStream_t s);
 
 // Classifier on the matrix cores, then the local error signal, for up to
 // kMaxClsLayers layers in one launch (ceil(n / 16) work-groups per layer).

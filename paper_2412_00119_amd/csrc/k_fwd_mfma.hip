@@ -146,18 +146,21 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   }
   const int m0 = mt * TM, n0 = nt * TN;
 
-  // For the fused selection: thread (r, w) fetches word w of the tile's
-  // columns of rho^{y^mu} for tile row r (pattern m0 + r) from the rows
-  // gathered at the start of the step, before the operand loads start (the
-  // compiler does not count direct-to-LDS loads, so a register load issued
-  // among them would make it wait for all of them).  The load is
-  // unconditional (indices clamped; when the selection is not fused the
-  // launcher points it at valid memory with a zero row stride).
+  // The step statistics start at zero (the first forward of a step zeroes
+  // them; the classifiers add to them after every forward is done).
+  if (p.zero != nullptr && blockIdx.x == 0)
+    for (int i = tid; i < p.nzero; i += 256) p.zero[i] = 0;
+
+  // For the fused selection thread (r, w) needs word w of the tile's
+  // columns of rho^{y^mu} = P_l[y^mu] for tile row r (pattern m0 + r).  The
+  // label is loaded right after the first operand loads (newer than them,
+  // so the prologue does not wait for it), the word of P_l once the K loop
+  // is done (see there).  Both loads are unconditional (indices clamped;
+  // when the selection is not fused the launcher points them at valid
+  // memory).
   const int pr = tid >> 1, pw = tid & 1;
   const int pm = m0 + pr, pwg = (n0 >> 6) + pw;
   const bool pvalid = p.mode == kFwdFusedSelect && pm < p.M && pwg < p.words_out;
-  const uint64_t prow = p.rho[(size_t)min(pm, p.M - 1) * p.ldr + min(pwg, p.pw_max)];
-  __builtin_amdgcn_sched_barrier(0);
 
   // Loads: a wave moves rows 32*wave .. 32*wave+31 of each operand.  Lane l
   // of instruction h fills LDS bytes UNIT*l of its kRowsPerDma rows: row
@@ -268,6 +271,8 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   issue(min(1, klast), s1);
   issue(min(2, klast), s2);
   __builtin_amdgcn_sched_barrier(0);
+  const int ylab = p.y[min(pm, p.M - 1) * p.ystride];
+  __builtin_amdgcn_sched_barrier(0);
   Ops r0, r1;
   wait_vm<kIssue * (kStages - 2)>();   // this wave's loads of step 0 are done
   __builtin_amdgcn_s_barrier();        // every wave's loads of step 0 have landed
@@ -316,12 +321,13 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     }
   }
   if (nfull < nks) compute_tail(r0, nfull);
-  sP[pw][pr] = pvalid ? prow : 0ull;
-  // A plain barrier after the LDS writes: a __syncthreads fence would also
-  // wait for the repeated loads of the last steps, which land during the
-  // epilogue instead (and are waited for before the wave ends).
-  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0) only
-  __builtin_amdgcn_s_barrier();
+  // The rho word, loaded while the last MFMAs drain (a register load that
+  // depends on the label, issued among the direct-to-LDS loads, would be
+  // waited for together with all of them).
+  __builtin_amdgcn_sched_barrier(0);
+  const int yl = min(max(ylab, 0), p.c - 1);   // stay inside P on a bad label
+  const uint64_t prow = p.P[(size_t)yl * p.ldp + min(pwg, p.pw_max)];
+  __builtin_amdgcn_sched_barrier(0);
 
   // ---- epilogue ---------------------------------------------------------------
   // lane holds z for column n0 + wn*64 + j*32 + (lane & 31) and rows
@@ -358,6 +364,15 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
       if (m < p.M && cw < 2 * p.words_out) ab32[(size_t)m * 2 * p.words_out + cw] = h ? bhi : blo;
     }
   }
+
+  // The rho words reach every wave through LDS, after the sign bits (the
+  // load of P_l overlaps them).  A plain barrier after the LDS writes: a
+  // __syncthreads fence would also wait for the repeated loads of the last
+  // steps, which land during the epilogue instead (and are waited for
+  // before the wave ends).
+  sP[pw][pr] = pvalid ? prow : 0ull;
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0) only
+  __builtin_amdgcn_s_barrier();
 
   if (p.mode == kFwdFusedSelect) {
     const int gcol0 = n0 + wn * 64;   // the wave's 64 columns are one group
@@ -426,22 +441,6 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   wait_vm<0>();   // the repeated loads write LDS: they land before the wave ends
 }
 
-// Zeroes the statistics and, for each listed layer, gathers the rows
-// rho^{y^mu} of P_l of the batch, one thread per 64-bit word (blockIdx.y =
-// 0: statistics; 1 + i: layer i).
-__global__ __launch_bounds__(256) void step_prep_kernel(PrepArgs p) {
-  const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (blockIdx.y == 0) {
-    if (p.zero != nullptr && t < p.nzero) p.zero[t] = 0;
-    return;
-  }
-  const PrepLayer &L = p.L[blockIdx.y - 1];
-  if (t >= (long long)p.n * L.words_out) return;
-  const int mu = (int)(t / L.words_out), w = (int)(t % L.words_out);
-  const int yl = min(max(p.y[mu], 0), p.c - 1);   // stay inside P on a bad label
-  L.rho[t] = L.P[(size_t)yl * L.words_out + w];
-}
-
 }  // namespace
 
 hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s) {
@@ -451,10 +450,15 @@ hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s) {
   a.nt_n = (a.N + TN - 1) / TN;
   a.xcd_remap = (a.nt_n % 8 == 0) ? 1 : 0;
   if (a.mode == kFwdFusedSelect) {
+    if (a.y == nullptr || a.P == nullptr || a.c < 1) return hipErrorInvalidValue;
     a.pw_max = a.words_out - 1;
-  } else {   // the kernel's rho load reads A instead (always valid)
-    a.rho = a.A;
-    a.ldr = 0;
+    a.ystride = 1;
+  } else {   // the label and rho loads read A instead (always valid)
+    a.y = reinterpret_cast<const int32_t *>(a.A);
+    a.ystride = 0;
+    a.P = a.A;
+    a.ldp = 0;
+    a.c = 1;
     a.pw_max = 0;
   }
   // rows start on 16-byte boundaries when the bases are 16-byte aligned and
@@ -465,14 +469,6 @@ hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s) {
     hipLaunchKernelGGL(fwd_fp4_kernel<16>, dim3(a.nt_m * a.nt_n), dim3(256), 0, s, a);
   else
     hipLaunchKernelGGL(fwd_fp4_kernel<4>, dim3(a.nt_m * a.nt_n), dim3(256), 0, s, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_step_prep(const PrepArgs &a, hipStream_t s) {
-  long long need = a.nzero;
-  for (int i = 0; i < a.nl; ++i) need = std::max(need, (long long)a.n * a.L[i].words_out);
-  if (need <= 0) return hipSuccess;
-  hipLaunchKernelGGL(step_prep_kernel, dim3((unsigned)((need + 255) / 256), 1 + a.nl), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
