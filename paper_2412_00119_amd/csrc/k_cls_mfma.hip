@@ -131,7 +131,33 @@ __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
       }
       __syncthreads();
       const int nsteps = min(kChunk, w32 - kw0 + 3) / 4;   // K steps of 4 words in this chunk
-      if (cg * PB < nb) {   // the wave has a class block in range
+      if (cg * PB < nb && nsteps == kChunk / 4) {
+        // a whole chunk: every operand word of the wave's K steps is read
+        // from LDS first, so the reads overlap instead of queueing behind
+        // each step's MFMAs
+        constexpr int kSteps = kChunk / 4 / KG;
+        uint32_t wa[kSteps], wb[kSteps][PB];
+#pragma unroll
+        for (int s = 0; s < kSteps; ++s) {
+          const int wl = 4 * (kg + s * KG) + q;
+          wa[s] = sA[lr * kStride + wl];
+#pragma unroll
+          for (int j = 0; j < PB; ++j) wb[s][j] = sP[((cg * PB + j) * 16 + lr) * kStride + wl];
+        }
+#pragma unroll
+        for (int s = 0; s < kSteps; ++s) {
+          const int wl = 4 * (kg + s * KG) + q;
+          const int nv = min(max(Lr.K - 32 * (kw0 + wl), 0), 32);
+          const uint32_t valid = nv == 32 ? 0xFFFFFFFFu : ((1u << nv) - 1u);
+          const uint4 av = fp4x32_permuted(wa[s]);
+#pragma unroll
+          for (int j = 0; j < PB; ++j)
+            if (cg * PB + j < nb) {
+              const uint4 bv = valid == 0xFFFFFFFFu ? fp4x32_permuted(wb[s][j]) : fp4x32_permuted_masked(wb[s][j], valid);
+              acc[j] = mfma_fp4(av, bv, acc[j]);
+            }
+        }
+      } else if (cg * PB < nb) {   // the wave has a class block in range
         for (int ks = kg; ks < nsteps; ks += KG) {
           const int wl = 4 * ks + q;   // the lane's word of the step, in the chunk
           // elements 32 (kw0 + wl) .. +31; those past K are padding (0 in fp4)
