@@ -124,6 +124,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   constexpr int kSlot = (TM + TN) * KB;
   __shared__ __align__(16) uint8_t s0[kSlot], s1[kSlot], s2[kSlot], s3[kSlot];
   __shared__ uint64_t sP[2][TM];       // rho^{y^mu} bits of the tile's 128 columns, per group
+  __shared__ int32_t sY[TM];           // labels of the tile's rows
   static_assert(kStages == 4, "one named array per slot");
   constexpr int kRowsPerDma = 64 * UNIT / KB;     // rows per load instruction: 16 or 4
   constexpr int kDma = 32 / kRowsPerDma;          // instructions per operand per wave and step
@@ -153,11 +154,12 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
 
   // For the fused selection thread (r, w) needs word w of the tile's
   // columns of rho^{y^mu} = P_l[y^mu] for tile row r (pattern m0 + r).  The
-  // label is loaded right after the first operand loads (newer than them,
-  // so the prologue does not wait for it), the word of P_l once the K loop
-  // is done (see there).  Both loads are unconditional (indices clamped;
-  // when the selection is not fused the launcher points them at valid
-  // memory).
+  // labels of the tile's rows come with the first operand loads, as a
+  // direct-to-LDS load of wave 0 (a register load among the direct-to-LDS
+  // loads would make the compiler wait for all of them before its use), and
+  // the word of P_l is loaded once they have landed, to be used after the
+  // K loop.  Both loads are unconditional (indices clamped; when the
+  // selection is not fused the launcher points them at valid memory).
   const int pr = tid >> 1, pw = tid & 1;
   const int pm = m0 + pr, pwg = (n0 >> 6) + pw;
   const bool pvalid = p.mode == kFwdFusedSelect && pm < p.M && pwg < p.words_out;
@@ -267,16 +269,21 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   const int nks = (p.K + 511) / 512;
   const int nfull = p.K / 512;      // steps with no element past K
   const int klast = nks - 1;        // nks >= 1
+  if (wave == 0) {   // labels first: the oldest loads, covered by the prologue's wait
+#pragma unroll
+    for (int h = 0; h < TM / 64; ++h)
+      dma<4>(p.y + (size_t)min(m0 + 64 * h + lane, p.M - 1) * p.ystride, sY + 64 * h);
+  }
   issue(0, s0);
   issue(min(1, klast), s1);
   issue(min(2, klast), s2);
   __builtin_amdgcn_sched_barrier(0);
-  const int ylab = p.y[min(pm, p.M - 1) * p.ystride];
-  __builtin_amdgcn_sched_barrier(0);
   Ops r0, r1;
-  wait_vm<kIssue * (kStages - 2)>();   // this wave's loads of step 0 are done
+  wait_vm<kIssue * (kStages - 2)>();   // this wave's loads of step 0 (and wave 0's labels) are done
   __builtin_amdgcn_s_barrier();        // every wave's loads of step 0 have landed
   read(r0, s0);
+  const int yl = min(max(sY[pr], 0), p.c - 1);   // stay inside P on a bad label
+  const uint64_t prow = p.P[(size_t)yl * p.ldp + min(pwg, p.pw_max)];
   __builtin_amdgcn_sched_barrier(0);
   // The sched_barrier(0) fences pin the order of the phases; otherwise the
   // scheduler sinks the read-ahead to its use and the LDS latency reappears.
@@ -321,13 +328,6 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     }
   }
   if (nfull < nks) compute_tail(r0, nfull);
-  // The rho word, loaded while the last MFMAs drain (a register load that
-  // depends on the label, issued among the direct-to-LDS loads, would be
-  // waited for together with all of them).
-  __builtin_amdgcn_sched_barrier(0);
-  const int yl = min(max(ylab, 0), p.c - 1);   // stay inside P on a bad label
-  const uint64_t prow = p.P[(size_t)yl * p.ldp + min(pwg, p.pw_max)];
-  __builtin_amdgcn_sched_barrier(0);
 
   // ---- epilogue ---------------------------------------------------------------
   // lane holds z for column n0 + wn*64 + j*32 + (lane & 31) and rows
@@ -365,8 +365,8 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     }
   }
 
-  // The rho words reach every wave through LDS, after the sign bits (the
-  // load of P_l overlaps them).  A plain barrier after the LDS writes: a
+  // The rho words reach every wave through LDS.  A plain barrier after the
+  // LDS writes: a
   // __syncthreads fence would also wait for the repeated loads of the last
   // steps, which land during the epilogue instead (and are waited for
   // before the wave ends).
