@@ -38,6 +38,16 @@ project's design notes):
   R13 all layers use the weights from before the step (the forward of layer
       l+1 reads a_l, which the update of layer l does not change).
   R14 labels are 0-based.
+  R15 the epoch loop (Algorithm 1) runs over the full mini-batches of a
+      given order of the training set; E^e is the fraction of those
+      samples whose last-layer local classifier was wrong during the epoch
+      (its 01-loss, counted as each batch is trained on), and p_r becomes
+      p_r * sqrt(E^e) after the epoch; an epoch with no full batch leaves
+      p_r unchanged.
+  R16 early exit (Section 3.1 names the strategy, not a rule): a pattern
+      exits at the first layer whose local classifier has a margin tau of
+      at least ceil(r * K_l), the training-time robustness test, and at the
+      last layer otherwise; its prediction is that layer's.
 
 Random numbers come from Philox4x32-10 (``oracle.philox``) keyed by the
 64-bit seed (k0 = low word, k1 = high word), with counter
@@ -391,6 +401,54 @@ def forward(state: State, x: np.ndarray) -> List[np.ndarray]:
     for l in range(1, state.cfg.n_layers + 1):
         a = activation(preactivation(a, state.W(l)))
         out.append(local_output(a, state.P[l - 1]))
+    return out
+
+
+@dataclass
+class EpochResult:
+    p_r: float            # p_r * sqrt(E^e): the probability for the next epoch
+    error_fraction: float  # E^e
+    stats: np.ndarray      # int64 [batches][L][4], each step's layer counts
+    steps: int             # full batches trained
+
+
+def train_epoch(state: State, x: np.ndarray, y: np.ndarray, order: np.ndarray, batch: int,
+                t0: int, p_r: float) -> EpochResult:
+    """One pass of Algorithm 1's epoch loop (its lines 4-20) and the rescale of
+    line 21 (Section 3.4), R15: the full batches order[b*batch:(b+1)*batch]
+    of the training set x (int8 ±1 [N][K_0]), y, trained with steps t0 + b,
+    all at the given p_r."""
+    order = np.asarray(order, dtype=np.int64)
+    nb = len(order) // batch
+    wrong = 0
+    stats = []
+    for b in range(nb):
+        idx = order[b * batch:(b + 1) * batch]
+        traces = train_step(state, x[idx], np.asarray(y)[idx], t0 + b, p_r)
+        wrong += int(traces[-1].err.sum())
+        stats.append(np.stack([tr.stats for tr in traces]))
+    if nb == 0:
+        return EpochResult(p_r, float("nan"), np.zeros((0, state.cfg.n_layers, 4), np.int64), 0)
+    e = wrong / (nb * batch)
+    return EpochResult(p_r * math.sqrt(e), e, np.stack(stats), nb)
+
+
+def early_exit(state: State, x: np.ndarray, y: np.ndarray) -> np.ndarray:
+    """Per layer l (rows): correct predictions of its local classifier, the
+    patterns that exit at l, and how many of those exits are correct (R16).
+    int64 [L][3]."""
+    cfg = state.cfg
+    y = np.asarray(y)
+    n = len(y)
+    out = np.zeros((cfg.n_layers, 3), dtype=np.int64)
+    left = np.ones(n, dtype=bool)           # not exited yet
+    for l, yhat in enumerate(forward(state, x), start=1):
+        pred, tau, err, _ = local_error(yhat, y, robustness_threshold(cfg.robustness, cfg.widths[l]))
+        out[l - 1, 0] = int((~err).sum())
+        here = left & ((tau >= robustness_threshold(cfg.robustness, cfg.widths[l])) | (l == cfg.n_layers))
+        out[l - 1, 1] = int(here.sum())
+        out[l - 1, 2] = int((here & ~err).sum())
+        left &= ~here
     return out
 
 
