@@ -208,6 +208,41 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
 int bmlp_eval(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int32_t n,
               int32_t *d_correct, void *stream);
 
+/* Early-exit evaluation.  Section 3.1 keeps the intermediate classifiers for
+ * early exit without fixing a rule; here a pattern exits at the first layer
+ * whose local output has a margin tau = top1 - top2 of at least
+ * ceil(r K_l) (the training-time robustness test passed), else at the last
+ * layer, and takes that layer's prediction.  Adds to d_counts, int32
+ * [L][3] (zeroed by the caller before the first batch), per layer l:
+ * [0] patterns whose layer-l classifier predicts the label (as bmlp_eval),
+ * [1] patterns that exit at layer l, [2] those exits whose prediction is
+ * the label.  0 <= n <= max_batch. */
+int bmlp_eval_exit(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int32_t n,
+                   int32_t *d_counts, void *stream);
+
+/* One epoch of Algorithm 1 (its epoch loop, lines 3-20) over a training set
+ * resident on the device: d_x_all bit rows [n_all][words(K_0)], d_y_all
+ * int32 [n_all].  d_order int32 [n_order] lists training-set indices (the
+ * caller's shuffle; indices outside [0, n_all) are clamped into range).
+ * The epoch trains the n_order / batch full batches
+ * order[b * batch .. b * batch + batch), b = 0, 1, ..., with step counters
+ * step0 + b, all at p_r (1 <= batch <= max_batch; the n_order % batch
+ * leftover indices are not trained on).  Each batch is gathered into the
+ * workspace and stepped exactly as bmlp_train_step; step b's counts go to
+ * d_stats + b * L * BMLP_STATS_STRIDE (int32 [n_order / batch][L][stride],
+ * 8-byte aligned).  Everything is enqueued on the stream; the call does not
+ * wait for it.  The epoch's error fraction E^e is the sum over the steps of
+ * the last layer's 01-loss count, divided by the trained samples; see
+ * bmlp_epoch_rescale for the p_r of the next epoch. */
+int bmlp_train_epoch(bmlp_ctx *ctx, const uint64_t *d_x_all, const int32_t *d_y_all, int32_t n_all,
+                     const int32_t *d_order, int32_t n_order, int32_t batch, uint64_t step0, double p_r,
+                     int32_t *d_stats, void *stream);
+
+/* The rescale at the end of an epoch (Algorithm 1 line 21, Section 3.4):
+ * p_r * sqrt(wrong / samples) in IEEE double, or p_r unchanged when no
+ * sample was trained on.  Host only. */
+double bmlp_epoch_rescale(double p_r, int64_t wrong, int64_t samples);
+
 /* Device pointers to H_l (bit-sliced, see bmlp_layer_info), W_l and P_l of
  * layer l (1..L) in the state. */
 int bmlp_layer_views(bmlp_ctx *ctx, int32_t l, uint8_t **d_h, uint64_t **d_w, uint64_t **d_p);

@@ -404,6 +404,14 @@ def forward(state: State, x: np.ndarray) -> List[np.ndarray]:
     return out
 
 
+def rescale(p_r: float, wrong: int, samples: int) -> float:
+    """p_r * sqrt(E^e) with E^e = wrong / samples (Algorithm 1 line 21,
+    Section 3.4); unchanged when no sample was trained on (R15)."""
+    if samples <= 0:
+        return p_r
+    return p_r * math.sqrt(wrong / samples)
+
+
 @dataclass
 class EpochResult:
     p_r: float            # p_r * sqrt(E^e): the probability for the next epoch
@@ -429,8 +437,7 @@ def train_epoch(state: State, x: np.ndarray, y: np.ndarray, order: np.ndarray, b
         stats.append(np.stack([tr.stats for tr in traces]))
     if nb == 0:
         return EpochResult(p_r, float("nan"), np.zeros((0, state.cfg.n_layers, 4), np.int64), 0)
-    e = wrong / (nb * batch)
-    return EpochResult(p_r * math.sqrt(e), e, np.stack(stats), nb)
+    return EpochResult(rescale(p_r, wrong, nb * batch), wrong / (nb * batch), np.stack(stats), nb)
 
 
 def early_exit(state: State, x: np.ndarray, y: np.ndarray) -> np.ndarray:

@@ -87,6 +87,9 @@ def lib() -> ctypes.CDLL:
             "bmlp_forward": (ctypes.c_int, [vp, vp, i32, vp, vp]),
             "bmlp_train_step": (ctypes.c_int, [vp, vp, vp, i32, u64, dbl, vp, vp]),
             "bmlp_eval": (ctypes.c_int, [vp, vp, vp, i32, vp, vp]),
+            "bmlp_eval_exit": (ctypes.c_int, [vp, vp, vp, i32, vp, vp]),
+            "bmlp_train_epoch": (ctypes.c_int, [vp, vp, vp, i32, vp, i32, i32, u64, dbl, vp, vp]),
+            "bmlp_epoch_rescale": (dbl, [dbl, ctypes.c_int64, ctypes.c_int64]),
             "bmlp_layer_views": (ctypes.c_int, [vp, i32, ctypes.POINTER(vp), ctypes.POINTER(vp),
                                                 ctypes.POINTER(vp)]),
             "bmlp_step_trace": (ctypes.c_int, [vp, i32, ctypes.POINTER(vp), ctypes.POINTER(vp),
@@ -181,6 +184,20 @@ def bmlp_train_step(ctx: int, d_x: int, d_y: int, n: int, step: int, p_r: float,
 
 def bmlp_eval(ctx: int, d_x: int, d_y: int, n: int, d_correct: int, stream: int):
     _check(lib().bmlp_eval(ctx, d_x, d_y, n, d_correct, stream), "bmlp_eval")
+
+
+def bmlp_eval_exit(ctx: int, d_x: int, d_y: int, n: int, d_counts: int, stream: int):
+    _check(lib().bmlp_eval_exit(ctx, d_x, d_y, n, d_counts, stream), "bmlp_eval_exit")
+
+
+def bmlp_train_epoch(ctx: int, d_x_all: int, d_y_all: int, n_all: int, d_order: int, n_order: int,
+                     batch: int, step0: int, p_r: float, d_stats: int, stream: int):
+    _check(lib().bmlp_train_epoch(ctx, d_x_all, d_y_all, n_all, d_order, n_order, batch, step0, p_r,
+                                  d_stats, stream), "bmlp_train_epoch")
+
+
+def bmlp_epoch_rescale(p_r: float, wrong: int, samples: int) -> float:
+    return lib().bmlp_epoch_rescale(p_r, wrong, samples)
 
 
 def bmlp_read_h(ctx: int, layer: int, d_out: int, stream: int):
@@ -296,6 +313,41 @@ class BMLP:
         bmlp_train_step(self.ctx, x_bits.data_ptr(), y.data_ptr(), n, int(step), float(p_r),
                         stats.data_ptr(), self._stream())
         return stats[:, :4]
+
+    def train_epoch(self, x_bits_all, y_all, order, step0: int, p_r: float, batch: Optional[int] = None):
+        """One epoch (Algorithm 1's epoch loop) over the full batches of ``order``
+        (int32 training-set indices) taken from the device-resident training set
+        ``x_bits_all`` (int64 bit rows [N][ceil(K_0/64)]), ``y_all`` (int32 [N]),
+        with steps step0, step0 + 1, ....  Returns (p_r for the next epoch,
+        E^e, int32 stats [batches][L][4]); E^e and the rescale need the
+        epoch's counts, so this waits for the stream."""
+        batch = self.max_batch if batch is None else int(batch)
+        t = self.torch
+        if x_bits_all.dim() != 2 or x_bits_all.shape[1] != words64(self.widths[0]) \
+                or x_bits_all.dtype != t.int64 or not x_bits_all.is_contiguous():
+            raise ValueError("x_bits_all must be contiguous int64 [N][ceil(K_0/64)]")
+        if y_all.dtype != t.int32 or y_all.shape != (x_bits_all.shape[0],) or not y_all.is_contiguous():
+            raise ValueError("y_all must be contiguous int32 [N]")
+        if order.dtype != t.int32 or order.dim() != 1 or not order.is_contiguous():
+            raise ValueError("order must be contiguous int32 [n_order]")
+        nb = order.shape[0] // batch
+        stats = t.zeros((max(nb, 1), self.n_layers, STATS_STRIDE), dtype=t.int32, device=self.device)
+        bmlp_train_epoch(self.ctx, x_bits_all.data_ptr(), y_all.data_ptr(), x_bits_all.shape[0],
+                         order.data_ptr(), order.shape[0], batch, int(step0), float(p_r), stats.data_ptr(),
+                         self._stream())
+        counts = stats[:nb, :, :4].cpu()   # waits for the stream
+        wrong = int(counts[:, -1, 0].sum()) if nb else 0
+        e = wrong / (nb * batch) if nb else float("nan")
+        return bmlp_epoch_rescale(float(p_r), wrong, nb * batch), e, counts
+
+    def eval_exit(self, x_bits, y, counts=None):
+        """Adds per layer [correct, exits, correct exits] of this batch to
+        ``counts`` (int32 [L][3]); see bmlp_eval_exit for the exit rule."""
+        n = self._batch(x_bits, y)
+        if counts is None:
+            counts = self.torch.zeros((self.n_layers, 3), dtype=self.torch.int32, device=self.device)
+        bmlp_eval_exit(self.ctx, x_bits.data_ptr(), y.data_ptr(), n, counts.data_ptr(), self._stream())
+        return counts
 
     def forward(self, x_bits):
         """Local outputs y_hat of every layer, int32 [L][n][c]."""

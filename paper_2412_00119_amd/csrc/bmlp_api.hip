@@ -168,6 +168,12 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
     lp.off_kstar = wo;
     wo = align256(wo + (size_t)nb * lp.groups * 2);
   }
+  p->off_flag = wo;   // early-exit flags [L][max_batch]
+  wo = align256(wo + (size_t)p->L * nb);
+  p->off_xb = wo;     // a gathered batch: bit rows [max_batch][words(K_0)] and labels
+  wo = align256(wo + (size_t)nb * p->layer[0].words_in * 8);
+  p->off_yb = wo;
+  wo = align256(wo + (size_t)nb * 4);
   p->ldz = 64 * words64(kmax);
   p->off_z = wo;
   wo = align256(wo + (size_t)nb * p->ldz * 2);
@@ -193,9 +199,11 @@ uint64_t reinforce_threshold(double p_r, int k) {
 
 bool use_mfma(const Plan &p) { return p.fwd_impl != BMLP_FWD_POPCOUNT; }
 
-// Forward of every layer for inference (y_hat out) or evaluation (counts).
+// Forward of every layer for inference (y_hat out) or evaluation (counts:
+// layer l adds to correct[cstride * (l - 1)]; with flags, each pattern's
+// flag of layer l goes to flags[(l - 1) * max_batch + mu]).
 int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32_t *yhat_out,
-                   const int32_t *y, int32_t *correct) {
+                   const int32_t *y, int32_t *correct, int cstride = 1, uint8_t *flags = nullptr) {
   ProfScope prof_scope{ctx};
   const Plan &p = ctx->plan;
   int32_t *yh_ws = reinterpret_cast<int32_t *>(ctx->ws + p.off_yhat);
@@ -220,9 +228,10 @@ int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32
       ClsLayer &c = cb.L[cb.nl++];
       c.A = reinterpret_cast<const uint64_t *>(ctx->ws + lp.off_a);
       c.P = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p);
-      c.words = lp.words_out; c.K = lp.k_out;
+      c.words = lp.words_out; c.K = lp.k_out; c.thr = lp.robust_thr;
       c.yhat = yhat_out ? yhat_out + (size_t)(l - 1) * n * p.c : yh_ws + (size_t)(l - 1) * p.max_batch * p.c;
-      c.correct = correct ? correct + (l - 1) : nullptr;
+      c.correct = correct ? correct + (size_t)cstride * (l - 1) : nullptr;
+      c.flag = flags ? flags + (size_t)(l - 1) * p.max_batch : nullptr;
       if (cb.nl == kMaxClsLayers || l == p.L) {
         BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_cls_fp4(cb, s));
         cb.nl = 0;
@@ -243,7 +252,9 @@ int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32
     BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s, launch_fill_i32(yh, n * p.c, lp.k_out, s));
     BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_cls_popcount(a, lp.words_out, lp.k_out, P, n, p.c, yh, p.c, s));
     if (correct)
-      BMLP_TIMED(ctx, BMLP_KERNEL_SELECT, s, launch_eval_count(yh, p.c, y, n, correct + (l - 1), s));
+      BMLP_TIMED(ctx, BMLP_KERNEL_SELECT, s,
+                 launch_eval_count(yh, p.c, y, n, correct + (size_t)cstride * (l - 1),
+                                   flags ? flags + (size_t)(l - 1) * p.max_batch : nullptr, lp.robust_thr, s));
     a_prev = a;
   }
   return BMLP_OK;
@@ -372,6 +383,26 @@ int bmlp_eval(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int32_t n,
   return forward_layers(ctx, d_x, n, as_stream(stream), nullptr, d_y, d_correct);
 }
 
+int bmlp_eval_exit(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int32_t n,
+                   int32_t *d_counts, void *stream) {
+  int st = check_ctx_batch(ctx, d_x, n);
+  if (st != BMLP_OK) return st;
+  if (n > 0 && (d_y == nullptr || d_counts == nullptr)) return BMLP_EINVAL;
+  if (n == 0) return BMLP_OK;
+  const Plan &p = ctx->plan;
+  hipStream_t s = as_stream(stream);
+  uint8_t *flags = ctx->ws + p.off_flag;
+  st = forward_layers(ctx, d_x, n, s, nullptr, d_y, d_counts, 3, flags);
+  if (st != BMLP_OK) return st;
+  BMLP_LAUNCH(launch_exit_count(flags, p.max_batch, p.L, n, d_counts, s));
+  return BMLP_OK;
+}
+
+double bmlp_epoch_rescale(double p_r, int64_t wrong, int64_t samples) {
+  if (samples <= 0) return p_r;
+  return p_r * sqrt((double)wrong / (double)samples);
+}
+
 int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int32_t n,
                     uint64_t step, double p_r, int32_t *d_stats, void *stream) {
   int st = check_ctx_batch(ctx, d_x, n);
@@ -480,6 +511,34 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
       BMLP_TIMED(ctx, BMLP_KERNEL_UPDATE, s, launch_update(ub, s));
       ub.nl = 0;
     }
+  }
+  return BMLP_OK;
+}
+
+int bmlp_train_epoch(bmlp_ctx *ctx, const uint64_t *d_x_all, const int32_t *d_y_all, int32_t n_all,
+                     const int32_t *d_order, int32_t n_order, int32_t batch, uint64_t step0, double p_r,
+                     int32_t *d_stats, void *stream) {
+  if (ctx == nullptr) return BMLP_EINVAL;
+  const Plan &p = ctx->plan;
+  if (batch < 1 || batch > p.max_batch || n_all < 0 || n_order < 0) return BMLP_ESHAPE;
+  const int nb = n_order / batch;
+  if (nb == 0) return BMLP_OK;
+  if (n_all < 1 || d_x_all == nullptr || d_y_all == nullptr || d_order == nullptr || d_stats == nullptr)
+    return BMLP_EINVAL;
+  if (reinterpret_cast<uintptr_t>(d_stats) & 7) return BMLP_EINVAL;
+  hipStream_t s = as_stream(stream);
+  uint64_t *xb = reinterpret_cast<uint64_t *>(ctx->ws + p.off_xb);
+  int32_t *yb = reinterpret_cast<int32_t *>(ctx->ws + p.off_yb);
+  for (int b = 0; b < nb; ++b) {
+    {
+      ProfScope prof_scope{ctx};
+      BMLP_TIMED(ctx, BMLP_KERNEL_OTHER, s,
+                 launch_gather_batch(d_x_all, d_y_all, n_all, p.layer[0].words_in, d_order + (size_t)b * batch,
+                                     batch, xb, yb, s));
+    }
+    const int st = bmlp_train_step(ctx, xb, yb, batch, step0 + (uint64_t)b, p_r,
+                                   d_stats + (size_t)b * BMLP_STATS_STRIDE * p.L, stream);
+    if (st != BMLP_OK) return st;
   }
   return BMLP_OK;
 }

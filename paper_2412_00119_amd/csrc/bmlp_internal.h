@@ -42,6 +42,7 @@ struct Plan {
   LayerPlan layer[BMLP_MAX_LAYERS];   // layer[l-1] describes layer l
   int ldz;                            // int16 elements per row of the z scratch
   size_t off_z, off_yhat;             // shared scratch in the workspace
+  size_t off_flag, off_xb, off_yb;    // early-exit flags; a gathered batch (epoch driver)
   size_t state_bytes, ws_bytes;
 };
 
@@ -107,6 +108,7 @@ struct ClsLayer {
   uint8_t *err, *upd;               // train
   int32_t *stats;                   // train: this layer's [4], adds [0] and [1]
   int32_t *correct;                 // eval: adds the correct count
+  uint8_t *flag;                    // eval, if set: per pattern, 1 = correct, 2 = tau >= thr
 };
 constexpr int kMaxClsLayers = 8;
 struct ClsBatch {
@@ -132,8 +134,17 @@ struct LossSelectArgs {
 hipError_t launch_loss_select(const LossSelectArgs &a, hipStream_t s);
 
 // correct[0] += #(argmax yhat == y)
+// flag, if set: per pattern, 1 = correct, 2 = the margin tau reaches thr
 hipError_t launch_eval_count(const int32_t *yhat, int c, const int32_t *y, int n, int32_t *correct,
-                             hipStream_t s);
+                             uint8_t *flag, int thr, hipStream_t s);
+// Early exits from the per-layer flags [L][ldf] (see launch_eval_count):
+// counts[l][1] += patterns whose first layer with flag & 2 (or the last
+// layer) is l, counts[l][2] += those of them with flag & 1.
+hipError_t launch_exit_count(const uint8_t *flags, int ldf, int L, int n, int32_t *counts, hipStream_t s);
+// Rows order[0..n) of a training set gathered into a batch: xb [n][words],
+// yb [n]; indices outside [0, n_all) are clamped into it.
+hipError_t launch_gather_batch(const uint64_t *x_all, const int32_t *y_all, int n_all, int words,
+                               const int32_t *order, int n, uint64_t *xb, int32_t *yb, hipStream_t s);
 
 // Clipped-Perceptron increments + reinforcement + clip + re-sign of up to
 // kMaxUpdLayers layers in one launch.

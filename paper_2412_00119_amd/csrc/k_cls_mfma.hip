@@ -228,6 +228,8 @@ __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
     if (lane == 0) {
       if (p.mode == kClsEval) {
         if (t.i1 == label) atomicAdd(&cnt[2], 1);
+        if (Lr.flag != nullptr)
+          Lr.flag[mu] = (uint8_t)((t.i1 == label ? 1 : 0) | ((t.v1 - t.v2) >= Lr.thr ? 2 : 0));
       } else {
         const bool err = t.i1 != label;
         const bool upd = err || (t.v1 - t.v2) < Lr.thr;

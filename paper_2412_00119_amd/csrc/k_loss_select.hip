@@ -115,7 +115,7 @@ __global__ __launch_bounds__(256) void loss_select_kernel(LossSelectArgs p) {
 }
 
 __global__ __launch_bounds__(256) void eval_count_kernel(const int32_t *yhat, int c, const int32_t *y,
-                                                         int n, int32_t *correct) {
+                                                         int n, int32_t *correct, uint8_t *flag, int thr) {
   __shared__ int cnt;
   if (threadIdx.x == 0) cnt = 0;
   __syncthreads();
@@ -123,10 +123,51 @@ __global__ __launch_bounds__(256) void eval_count_kernel(const int32_t *yhat, in
   const int lane = threadIdx.x & 63;
   if (mu < n) {
     const Top2 t = wave_top2(yhat + (size_t)mu * c, c, lane);
-    if (lane == 0 && t.i1 == y[mu]) atomicAdd(&cnt, 1);
+    const bool ok = t.i1 == y[mu];
+    if (lane == 0 && ok) atomicAdd(&cnt, 1);
+    if (lane == 0 && flag != nullptr) flag[mu] = (uint8_t)((ok ? 1 : 0) | ((t.v1 - t.v2) >= thr ? 2 : 0));
   }
   __syncthreads();
   if (threadIdx.x == 0 && cnt) atomicAdd(correct, cnt);
+}
+
+// Early exit (one thread per pattern): the first layer whose flag has bit 1
+// (margin reached), else the last layer.  Counts gather per work-group in
+// LDS, then one atomic per nonzero counter.
+__global__ __launch_bounds__(256) void exit_count_kernel(const uint8_t *flags, int ldf, int L, int n,
+                                                         int32_t *counts) {
+  __shared__ int cnt[BMLP_MAX_LAYERS][2];
+  for (int i = threadIdx.x; i < L * 2; i += 256) cnt[i >> 1][i & 1] = 0;
+  __syncthreads();
+  const int mu = blockIdx.x * 256 + threadIdx.x;
+  if (mu < n) {
+    for (int l = 0; l < L; ++l) {
+      const uint8_t f = flags[(size_t)l * ldf + mu];
+      if ((f & 2) || l == L - 1) {
+        atomicAdd(&cnt[l][0], 1);
+        if (f & 1) atomicAdd(&cnt[l][1], 1);
+        break;
+      }
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < L * 2; i += 256) {
+    const int v = cnt[i >> 1][i & 1];
+    if (v) atomicAdd(counts + 3 * (i >> 1) + 1 + (i & 1), v);
+  }
+}
+
+// one thread per 64-bit word of the batch; the word-0 thread of a row also
+// copies its label
+__global__ __launch_bounds__(256) void gather_batch_kernel(const uint64_t *x_all, const int32_t *y_all,
+                                                           int n_all, int words, const int32_t *order, int n,
+                                                           uint64_t *xb, int32_t *yb) {
+  const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (long long)n * words) return;
+  const int i = (int)(t / words), w = (int)(t % words);
+  const int src = min(max(order[i], 0), n_all - 1);
+  xb[t] = x_all[(size_t)src * words + w];
+  if (w == 0) yb[i] = y_all[src];
 }
 
 }  // namespace
@@ -138,9 +179,26 @@ hipError_t launch_loss_select(const LossSelectArgs &a, hipStream_t s) {
 }
 
 hipError_t launch_eval_count(const int32_t *yhat, int c, const int32_t *y, int n, int32_t *correct,
-                             hipStream_t s) {
+                             uint8_t *flag, int thr, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(eval_count_kernel, dim3((n + 3) / 4), dim3(256), 0, s, yhat, c, y, n, correct);
+  hipLaunchKernelGGL(eval_count_kernel, dim3((n + 3) / 4), dim3(256), 0, s, yhat, c, y, n, correct, flag, thr);
+  return hipGetLastError();
+}
+
+hipError_t launch_exit_count(const uint8_t *flags, int ldf, int L, int n, int32_t *counts, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (L < 1 || L > BMLP_MAX_LAYERS) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(exit_count_kernel, dim3((n + 255) / 256), dim3(256), 0, s, flags, ldf, L, n, counts);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_batch(const uint64_t *x_all, const int32_t *y_all, int n_all, int words,
+                               const int32_t *order, int n, uint64_t *xb, int32_t *yb, hipStream_t s) {
+  const long long total = (long long)n * words;
+  if (total <= 0) return hipSuccess;
+  if (n_all < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(gather_batch_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, x_all, y_all,
+                     n_all, words, order, n, xb, yb);
   return hipGetLastError();
 }
 

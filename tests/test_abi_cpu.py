@@ -131,3 +131,10 @@ def test_h_planes_hold_offset_values(bound, planes):
     assert i.h_planes == planes
     assert (1 << planes) > bound >= (1 << (planes - 1))
     assert i.ld_h == 4 * planes * i.h_ps and i.h_ps == 16
+
+
+@pytest.mark.parametrize("p_r,wrong,samples", [(0.5, 317, 1024), (0.5, 0, 48 * 1024), (0.5, 1024, 1024),
+                                                (0.123456789, 12345, 49152), (2.0, 7, 9), (0.5, 3, 0)])
+def test_epoch_rescale_matches_oracle(p_r, wrong, samples):
+    # host arithmetic in IEEE double on both sides: equal to the last bit
+    assert B.bmlp_epoch_rescale(p_r, wrong, samples) == ob.rescale(p_r, wrong, samples)
