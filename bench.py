@@ -248,6 +248,31 @@ def main():
                      "update_hbm_frac": upd_gbs / HBM_PEAK_GBS if upd_gbs else None,
                      "update_bytes_per_launch": update_bytes(w)}
 
+    # One epoch through the epoch driver (bmlp_train_epoch: each batch
+    # gathered from the device-resident training set, then stepped), over
+    # the batches made above in a seeded order, timed with events on the
+    # library's stream; then the error fraction and the rescaled p_r.
+    epoch = None
+    if not w.streamed and len(xs) > 1:
+        x_all, y_all = torch.cat(xs), torch.cat(ys)
+        order = torch.from_numpy(synth.epoch_order(w, 1, x_all.shape[0]).astype(np.int32)).cuda()
+        nb = x_all.shape[0] // w.batch
+        ep_stats = torch.zeros((nb, w.n_layers, B.STATS_STRIDE), dtype=torch.int32, device="cuda")
+        torch.cuda.synchronize()
+        ev0.record()
+        B.bmlp_train_epoch(net.ctx, x_all.data_ptr(), y_all.data_ptr(), x_all.shape[0], order.data_ptr(),
+                           order.shape[0], w.batch, t, w.p_r, ep_stats.data_ptr(), net._stream())
+        ev1.record()
+        torch.cuda.synchronize()
+        ep_ms = ev0.elapsed_time(ev1)
+        wrong = int(ep_stats[:, -1, 0].sum())
+        epoch = {"samples": nb * w.batch, "steps": nb, "ms": ep_ms,
+                 "samples_per_s": nb * w.batch / (ep_ms / 1e3), "error_fraction": wrong / (nb * w.batch),
+                 "p_r_next": B.bmlp_epoch_rescale(w.p_r, wrong, nb * w.batch)}
+        t += nb
+        log(f"one epoch through the epoch driver: {nb} steps in {ep_ms:.3f} ms "
+            f"({epoch['samples_per_s']:.4g} samples/s), E = {epoch['error_fraction']:.4f}")
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the oracle on the host ...")
@@ -275,6 +300,7 @@ def main():
         "mac_per_step": fwd_macs + cls_macs,
         "roofline": roofline,
         "step_roofline": step_roofline,
+        "epoch": epoch,
         "kernels": kernels,
         "cpu_baseline": cpu,
     }

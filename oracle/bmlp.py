@@ -38,13 +38,15 @@ project's design notes):
   R13 all layers use the weights from before the step (the forward of layer
       l+1 reads a_l, which the update of layer l does not change).
   R14 labels are 0-based.
-  R15 the epoch loop (Algorithm 1) runs over the full mini-batches of a
+  R15 (the bound B = 127 of workloads that give none belongs to the
+      workload definitions, not to this module.)
+  R16 the epoch loop (Algorithm 1) runs over the full mini-batches of a
       given order of the training set; E^e is the fraction of those
       samples whose last-layer local classifier was wrong during the epoch
       (its 01-loss, counted as each batch is trained on), and p_r becomes
       p_r * sqrt(E^e) after the epoch; an epoch with no full batch leaves
       p_r unchanged.
-  R16 early exit (Section 3.1 names the strategy, not a rule): a pattern
+  R17 early exit (Section 3.1 names the strategy, not a rule): a pattern
       exits at the first layer whose local classifier has a margin tau of
       at least ceil(r * K_l), the training-time robustness test, and at the
       last layer otherwise; its prediction is that layer's.
@@ -406,7 +408,7 @@ def forward(state: State, x: np.ndarray) -> List[np.ndarray]:
 
 def rescale(p_r: float, wrong: int, samples: int) -> float:
     """p_r * sqrt(E^e) with E^e = wrong / samples (Algorithm 1 line 21,
-    Section 3.4); unchanged when no sample was trained on (R15)."""
+    Section 3.4); unchanged when no sample was trained on (R16)."""
     if samples <= 0:
         return p_r
     return p_r * math.sqrt(wrong / samples)
@@ -423,7 +425,7 @@ class EpochResult:
 def train_epoch(state: State, x: np.ndarray, y: np.ndarray, order: np.ndarray, batch: int,
                 t0: int, p_r: float) -> EpochResult:
     """One pass of Algorithm 1's epoch loop (its lines 4-20) and the rescale of
-    line 21 (Section 3.4), R15: the full batches order[b*batch:(b+1)*batch]
+    line 21 (Section 3.4), R16: the full batches order[b*batch:(b+1)*batch]
     of the training set x (int8 ±1 [N][K_0]), y, trained with steps t0 + b,
     all at the given p_r."""
     order = np.asarray(order, dtype=np.int64)
@@ -442,7 +444,7 @@ def train_epoch(state: State, x: np.ndarray, y: np.ndarray, order: np.ndarray, b
 
 def early_exit(state: State, x: np.ndarray, y: np.ndarray) -> np.ndarray:
     """Per layer l (rows): correct predictions of its local classifier, the
-    patterns that exit at l, and how many of those exits are correct (R16).
+    patterns that exit at l, and how many of those exits are correct (R17).
     int64 [L][3]."""
     cfg = state.cfg
     y = np.asarray(y)

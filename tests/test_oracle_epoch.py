@@ -1,5 +1,5 @@
 """Pins the oracle's epoch loop and p_r rescale (Algorithm 1, Section 3.4;
-reading R15) and its early-exit evaluation (Section 3.1; reading R16)."""
+reading R16) and its early-exit evaluation (Section 3.1; reading R17)."""
 import math
 
 import numpy as np
