@@ -33,7 +33,8 @@ project's design notes):
   R9  H and P start uniform on {-1, +1}; B is odd, so h stays odd.
   R10 reinforcement runs once per step on every hidden weight of a layer,
       only when M_l is not empty, after the CP increments.
-  R11 the K in the reinforcement probability is K_l, as printed.
+  R11 the K in the reinforcement probability is K_l, as printed (the
+      fan_in_reinforce variant uses K_{l-1}).
   R12 Uniform(0,1) is a 32-bit draw u, and "p < q" is u < ceil(q * 2^32).
   R13 all layers use the weights from before the step (the forward of layer
       l+1 reads a_l, which the update of layer l does not change).
@@ -208,6 +209,10 @@ class Config:
     group_size: int = 64            # gamma; 0 = gamma* per layer
     robustness: float = 0.25
     seed: int = 0
+    # method variants (each off by default)
+    fan_in_reinforce: bool = False   # K_{l-1} instead of K_l in the reinforcement probability
+    shared_classifier: bool = False  # one P for every layer (all K_l equal, Section 3.1)
+    saturate_z: bool = False         # z held in min(8, ceil(log2(2 K_{l-1}))) bits (Section 3.5)
 
     def __post_init__(self):
         self.widths = tuple(int(v) for v in self.widths)
@@ -220,6 +225,8 @@ class Config:
         for k in self.widths[1:]:
             if self.gamma(k) < 1 or k % self.gamma(k):
                 raise ValueError(f"group size must divide K_l={k}")
+        if self.shared_classifier and len(set(self.widths[1:])) != 1:
+            raise ValueError("a shared classifier needs every K_l equal")
 
     @property
     def n_layers(self) -> int:
@@ -254,11 +261,13 @@ def init_layer(cfg: Config, l: int):
 
 
 def init(cfg: Config) -> State:
+    """Every layer's H_l and P_l; with a shared classifier every layer uses
+    layer 1's P (Section 3.1)."""
     Hs, Ps = [], []
     for l in range(1, cfg.n_layers + 1):
         H, P = init_layer(cfg, l)
         Hs.append(H)
-        Ps.append(P)
+        Ps.append(Ps[0] if cfg.shared_classifier and l > 1 else P)
     return State(cfg, Hs, Ps)
 
 
@@ -300,6 +309,19 @@ def local_error(yhat: np.ndarray, y: np.ndarray, thr: int):
     err = pred != y
     upd = err | (tau < thr)
     return pred, tau, err, upd
+
+
+def z_bits(k_in: int) -> int:
+    """min(8, ceil(log2(2 K_{l-1}))) bits for z (Section 3.5)."""
+    return min(8, (2 * k_in - 1).bit_length())
+
+
+def saturate(z: np.ndarray, k_in: int) -> np.ndarray:
+    """z held in z_bits(K_{l-1}) two's-complement bits: clipped to
+    [-2^(b-1), 2^(b-1) - 1].  Its sign is that of z, so a_l is unchanged;
+    only the selection of Algorithm 2 sees the clipped magnitudes."""
+    b = z_bits(k_in)
+    return np.clip(z, -(1 << (b - 1)), (1 << (b - 1)) - 1)
 
 
 def select_easiest(z: np.ndarray, P: np.ndarray, y: np.ndarray, upd: np.ndarray, gamma: int) -> np.ndarray:
@@ -346,7 +368,7 @@ def reinforce(h: np.ndarray, mask: np.ndarray, bound: int) -> np.ndarray:
 @dataclass
 class LayerTrace:
     a: np.ndarray         # int8 ±1 [n][K_l]
-    z: np.ndarray         # int64 [n][K_l]
+    z: np.ndarray         # int64 [n][K_l], as Algorithm 2 sees it (saturated with saturate_z)
     yhat: np.ndarray      # int64 [n][c]
     pred: np.ndarray
     tau: np.ndarray
@@ -378,6 +400,8 @@ def train_step(state: State, x: np.ndarray, y: np.ndarray, t: int, p_r: float,
         W = state.W(l)
         z = preactivation(a_prev, W)
         a = activation(z)
+        if cfg.saturate_z:
+            z = saturate(z, kin)
         yhat = local_output(a, P)
         pred, tau, err, upd = local_error(yhat, y, robustness_threshold(cfg.robustness, kout))
         kstar = select_easiest(z, P, y, upd, gamma)
@@ -387,7 +411,8 @@ def train_step(state: State, x: np.ndarray, y: np.ndarray, t: int, p_r: float,
             # LayerUpdate / PerceptronUpdate run only when M_l is not empty.
             S = selection_matrix(kstar, P, y, gamma)
             h1 = clip(H.astype(np.int64) + cp_increment(S, a_prev), cfg.bound)
-            mask = reinforce_mask(cfg.seed, l, t, reinforce_threshold(p_r, kout), kin * kout, kin)
+            kq = kin if cfg.fan_in_reinforce else kout     # R11, or the fan-in variant
+            mask = reinforce_mask(cfg.seed, l, t, reinforce_threshold(p_r, kq), kin * kout, kin)
             nreinf = int(mask.sum())
             state.H[l - 1] = reinforce(h1, mask, cfg.bound).astype(np.int8)
         traces.append(LayerTrace(a, z, yhat, pred, tau, err, upd, kstar,

@@ -1,0 +1,88 @@
+"""Pins the oracle's method variants: K_{l-1} in the reinforcement
+probability (R11's alternative), one classifier shared by every layer
+(Section 3.1) and z held in min(8, ceil(log2(2 K_{l-1}))) bits
+(Section 3.5)."""
+import numpy as np
+import pytest
+
+import oracle.bmlp as ob
+from paper_2412_00119_amd.synth import random_pm1
+
+
+@pytest.mark.parametrize("fan_in", [False, True])
+def test_fan_in_reinforcement(fan_in):
+    # q(K=4) at p_r = 3 is above 1, so T saturates at 2^32 and every weight
+    # of the layer reinforces; q(K=40) is 0.38
+    assert ob.reinforce_threshold(3.0, 4) == 1 << 32
+    assert ob.reinforce_threshold(3.0, 40) < 1 << 31
+    cfg = ob.Config((4, 40), 2, 7, 8, 0.25, seed=3, fan_in_reinforce=fan_in)
+    st = ob.init(cfg)
+    rng = np.random.default_rng(1)
+    tr = ob.train_step(st, random_pm1((16, 4), rng), rng.integers(0, 2, 16), 0, 3.0)
+    assert tr[0].upd.any()
+    if fan_in:
+        assert tr[0].stats[3] == 4 * 40
+    else:
+        assert 0 < tr[0].stats[3] < 4 * 40
+
+
+def test_shared_classifier():
+    base = ob.init(ob.Config((20, 16, 16, 16), 3, 7, 4, 0.25, seed=5))
+    st = ob.init(ob.Config((20, 16, 16, 16), 3, 7, 4, 0.25, seed=5, shared_classifier=True))
+    for l in range(3):
+        np.testing.assert_array_equal(st.P[l], base.P[0])
+    with pytest.raises(ValueError):
+        ob.Config((20, 16, 8), 3, 7, 4, 0.25, shared_classifier=True)
+
+
+@pytest.mark.parametrize("k,bits", [(1, 1), (2, 2), (32, 6), (33, 7), (64, 7), (65, 8), (100, 8), (4096, 8)])
+def test_z_bits_closed_form(k, bits):
+    # ceil(log2(2K)) bits hold every z in [-K, K] but +K when 2K is a power
+    # of two; 8 is the cap
+    assert ob.z_bits(k) == bits
+
+
+def _brute_select(z, rho_rows, upd, gamma):
+    n, k = z.shape
+    out = -np.ones((n, k // gamma), dtype=np.int64)
+    for mu in range(n):
+        if not upd[mu]:
+            continue
+        for g in range(k // gamma):
+            best, babs = -1, None
+            for e in range(gamma):
+                kk = g * gamma + e
+                d = int(z[mu, kk]) * int(rho_rows[mu][kk])
+                if d < 0 and (babs is None or abs(int(z[mu, kk])) < babs):
+                    best, babs = e, abs(int(z[mu, kk]))
+            out[mu, g] = best
+    return out
+
+
+def test_saturated_selection_brute_force():
+    # W rows are +x0 and -x0 alternately, so z = +-300 on pattern x0: all
+    # saturate, to 127 and -128, and ties move
+    k_in, k_out = 300, 16
+    # r = 100 puts every pattern in M; for label 0 the classifier row makes
+    # perceptrons 1 (z = -300 -> -128) and 2 (z = +300 -> 127) the wrong
+    # ones: exact z picks 1, saturated z picks 2
+    cfg = ob.Config((k_in, k_out), 2, 7, 16, 100.0, seed=7, saturate_z=True)
+    exact = ob.Config((k_in, k_out), 2, 7, 16, 100.0, seed=7)
+    rng = np.random.default_rng(2)
+    x0 = random_pm1((1, k_in), rng)[0]
+    x = np.stack([x0] * 3 + list(random_pm1((5, k_in), rng)))
+    y = np.array([0, 1, 0, 1, 0, 1, 0, 1])
+    picks = []
+    for c in (cfg, exact):
+        st = ob.init(c)
+        st.H[0][:] = np.where(np.arange(k_out)[:, None] % 2 == 0, 1, -1) * x0[None, :]
+        st.P[0][0] = np.where(np.arange(k_out) % 2 == 0, 1, -1)
+        st.P[0][0, 1], st.P[0][0, 2] = 1, -1
+        tr = ob.train_step(st.copy(), x, y, 0, 0.0)[0]
+        z_exact = ob.preactivation(x, st.W(1))
+        zs = ob.saturate(z_exact, k_in) if c.saturate_z else z_exact
+        np.testing.assert_array_equal(tr.z, zs)
+        np.testing.assert_array_equal(tr.a, ob.activation(z_exact))
+        np.testing.assert_array_equal(tr.kstar, _brute_select(zs, st.P[0][y], tr.upd, 16))
+        picks.append(tr.kstar)
+    assert not np.array_equal(picks[0], picks[1])   # saturation changed a choice
