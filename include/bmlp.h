@@ -61,6 +61,21 @@ enum {
   BMLP_FWD_MFMA_FP4 = 2,  /* ±1 as e2m1 operands of the scaled fp4 MFMA: exact  */
 };
 
+/* Method variants (bmlp_config.variants, a bit set; 0 = the method as
+ * printed). */
+enum {
+  /* q_l = p_r sqrt(2 / (pi K_{l-1})): the fan-in instead of K_l in the
+   * reinforcement probability (Algorithm 3 prints K_l). */
+  BMLP_VARIANT_FAN_IN_REINFORCE = 1,
+  /* one classifier P for every layer, layer 1's (Section 3.1); needs every
+   * K_l (l >= 1) equal.  The state then holds P once. */
+  BMLP_VARIANT_SHARED_CLASSIFIER = 2,
+  /* Algorithm 2 on z held in min(8, ceil(log2(2 K_{l-1}))) two's-complement
+   * bits, i.e. clipped to [-2^(b-1), 2^(b-1) - 1] (Section 3.5); a_l keeps
+   * the sign of the exact z. */
+  BMLP_VARIANT_SATURATE_Z = 4,
+};
+
 /* Limits of this build. */
 #define BMLP_MAX_LAYERS 64
 #define BMLP_MAX_WIDTH 32767      /* |z| <= K_{l-1} must fit in int16          */
@@ -85,6 +100,7 @@ enum {
  *                pattern is updated when tau < ceil(r * K_l).
  *   seed         64-bit key of the Philox4x32-10 streams (init, reinforcement).
  *   fwd_impl     BMLP_FWD_* .
+ *   variants     0 or a bit set of BMLP_VARIANT_* .
  */
 typedef struct bmlp_config {
   int32_t n_layers;
@@ -96,7 +112,7 @@ typedef struct bmlp_config {
   double robustness;
   uint64_t seed;
   int32_t fwd_impl;
-  int32_t reserved;
+  int32_t variants;
 } bmlp_config;
 
 /*

@@ -28,6 +28,11 @@ BMLP_FWD_AUTO = 0
 BMLP_FWD_POPCOUNT = 1
 BMLP_FWD_MFMA_FP4 = 2
 
+# method variants (bmlp_config.variants)
+BMLP_VARIANT_FAN_IN_REINFORCE = 1
+BMLP_VARIANT_SHARED_CLASSIFIER = 2
+BMLP_VARIANT_SATURATE_Z = 4
+
 MAX_BATCH = 16384
 
 
@@ -51,7 +56,7 @@ class bmlp_config(ctypes.Structure):
         ("robustness", ctypes.c_double),
         ("seed", ctypes.c_uint64),
         ("fwd_impl", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("variants", ctypes.c_int32),
     ]
 
 
@@ -116,11 +121,11 @@ def lib() -> ctypes.CDLL:
 
 def make_config(widths: Sequence[int], n_classes: int, bound: int, max_batch: int,
                 group_size: int = 64, robustness: float = 0.25, seed: int = 0,
-                fwd_impl: int = BMLP_FWD_AUTO):
+                fwd_impl: int = BMLP_FWD_AUTO, variants: int = 0):
     """A bmlp_config plus the widths array it points to (keep both alive)."""
     arr = (ctypes.c_int32 * len(widths))(*[int(w) for w in widths])
     cfg = bmlp_config(len(widths) - 1, arr, n_classes, max_batch, bound, group_size,
-                      float(robustness), int(seed) & (2**64 - 1), fwd_impl, 0)
+                      float(robustness), int(seed) & (2**64 - 1), fwd_impl, int(variants))
     cfg._widths_keepalive = arr
     return cfg
 
@@ -241,7 +246,7 @@ class BMLP:
 
     def __init__(self, widths: Sequence[int], n_classes: int, bound: int, max_batch: int,
                  group_size: int = 64, robustness: float = 0.25, seed: int = 0,
-                 fwd_impl: int = BMLP_FWD_AUTO, device="cuda", state=None):
+                 fwd_impl: int = BMLP_FWD_AUTO, device="cuda", state=None, variants: int = 0):
         import torch
         self.torch = torch
         dev = torch.device(device)
@@ -253,7 +258,7 @@ class BMLP:
         self.n_classes = int(n_classes)
         self.max_batch = int(max_batch)
         self.cfg = make_config(self.widths, n_classes, bound, max_batch, group_size, robustness,
-                               seed, fwd_impl)
+                               seed, fwd_impl, variants)
         sb, wb = bmlp_state_bytes(self.cfg), bmlp_workspace_bytes(self.cfg)
         if sb == 0 or wb == 0:
             raise BmlpError(BMLP_ESHAPE, "configuration")

@@ -117,7 +117,11 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
   if (cfg->fwd_impl != BMLP_FWD_AUTO && cfg->fwd_impl != BMLP_FWD_POPCOUNT &&
       cfg->fwd_impl != BMLP_FWD_MFMA_FP4)
     return BMLP_EINVAL;
+  constexpr int kAllVariants =
+      BMLP_VARIANT_FAN_IN_REINFORCE | BMLP_VARIANT_SHARED_CLASSIFIER | BMLP_VARIANT_SATURATE_Z;
+  if (cfg->variants & ~kAllVariants) return BMLP_EINVAL;
   memset(p, 0, sizeof(*p));
+  p->variants = cfg->variants;
   p->L = cfg->n_layers;
   p->c = cfg->n_classes;
   p->max_batch = cfg->max_batch;
@@ -131,6 +135,7 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
     if (k < 1 || k > BMLP_MAX_WIDTH) return BMLP_ESHAPE;
     p->widths[l] = k;
     if (l > 0 && k > kmax) kmax = k;
+    if ((p->variants & BMLP_VARIANT_SHARED_CLASSIFIER) && l > 1 && k != p->widths[1]) return BMLP_ESHAPE;
   }
   const int nb = p->max_batch;
   size_t so = 0;
@@ -152,8 +157,12 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
     so = align256(so + (size_t)lp.k_out * lp.ld_h);
     lp.off_w = so;
     so = align256(so + (size_t)lp.k_out * lp.words_in * 8);
-    lp.off_p = so;
-    so = align256(so + (size_t)p->c * lp.words_out * 8);
+    if ((p->variants & BMLP_VARIANT_SHARED_CLASSIFIER) && l > 1) {
+      lp.off_p = p->layer[0].off_p;   // layer 1's P serves every layer
+    } else {
+      lp.off_p = so;
+      so = align256(so + (size_t)p->c * lp.words_out * 8);
+    }
   }
   p->state_bytes = so;
   size_t wo = 0;
@@ -198,6 +207,13 @@ uint64_t reinforce_threshold(double p_r, int k) {
 }
 
 bool use_mfma(const Plan &p) { return p.fwd_impl != BMLP_FWD_POPCOUNT; }
+
+// min(8, ceil(log2(2 K))) bits: the width of z in the saturating variant
+int z_bits(int k) {
+  int b = 0;
+  while ((1 << b) < 2 * k) ++b;
+  return b < 8 ? b : 8;
+}
 
 // Forward of every layer for inference (y_hat out) or evaluation (counts:
 // layer l adds to correct[cstride * (l - 1)]; with flags, each pattern's
@@ -290,7 +306,8 @@ int setup(const bmlp_config *cfg, void *d_state, void *d_ws, void *stream, bmlp_
     uint64_t *P = reinterpret_cast<uint64_t *>(ctx->state + lp.off_p);
     hipError_t e = launch_init_h(H, lp.ld_h, lp.h_ps, p.bound, W, lp.words_in, lp.k_in, lp.k_out, p.seed, l,
                                  from_h, s);
-    if (e == hipSuccess && !from_h) e = launch_init_p(P, lp.words_out, lp.k_out, p.c, p.seed, l, s);
+    const bool own_p = l == 1 || !(p.variants & BMLP_VARIANT_SHARED_CLASSIFIER);
+    if (e == hipSuccess && !from_h && own_p) e = launch_init_p(P, lp.words_out, lp.k_out, p.c, p.seed, l, s);
     if (e != hipSuccess) {
       delete ctx;
       return hip_fail(e, "init");
@@ -436,6 +453,14 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
     ls.y = d_y; ls.n = n;
     ls.k_out = lp.k_out; ls.gamma = lp.gamma; ls.groups = lp.groups; ls.thr = lp.robust_thr;
     ls.err = err; ls.upd = upd; ls.kstar = kstar; ls.ldk = p.max_batch; ls.stats = stats;
+    // the selection's view of z: clipped to z_bits(K_{l-1}) bits as a variant
+    int zlo = -65536, zhi = 65535;
+    if (p.variants & BMLP_VARIANT_SATURATE_Z) {
+      const int b = z_bits(lp.k_in);
+      zlo = -(1 << (b - 1));
+      zhi = (1 << (b - 1)) - 1;
+    }
+    ls.zlo = zlo; ls.zhi = zhi;
     if (mfma) {
       const bool fused = lp.gamma == 64;
       // Algorithm 1 lines 8-9, and Algorithm 2's choice when fused
@@ -447,6 +472,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
       f.mode = fused ? kFwdFusedSelect : kFwdWriteZ;
       f.kstar = kstar; f.ldk = p.max_batch;
       f.y = d_y; f.c = p.c; f.P = P; f.ldp = lp.words_out;
+      f.zlo = (float)zlo; f.zhi = (float)zhi;
       f.z = z; f.ldz = p.ldz;
       if (l == 1) {   // the step statistics start at zero
         f.zero = d_stats; f.nzero = BMLP_STATS_STRIDE * p.L;
@@ -504,7 +530,8 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
     u.stats = d_stats + BMLP_STATS_STRIDE * (l - 1);
     u.ld_h = lp.ld_h; u.h_ps = lp.h_ps; u.nw32 = 2 * lp.words_in; u.words_out = lp.words_out;
     u.k_in = lp.k_in; u.groups = lp.groups; u.gamma = lp.gamma;
-    const uint64_t T = reinforce_threshold(p_r, lp.k_out);
+    // R11: K_l, or the fan-in K_{l-1} as a variant
+    const uint64_t T = reinforce_threshold(p_r, (p.variants & BMLP_VARIANT_FAN_IN_REINFORCE) ? lp.k_in : lp.k_out);
     u.t_hi = (uint32_t)(T >> 24); u.t_lo = (uint32_t)(T & 0xFFFFFFu);
     u.ctr1 = (uint32_t)(l - 1);
     if (ub.nl == kMaxUpdLayers || l == p.L) {

@@ -35,7 +35,7 @@ struct LayerPlan {
 };
 
 struct Plan {
-  int L, c, max_batch, bound, fwd_impl;
+  int L, c, max_batch, bound, fwd_impl, variants;
   double r;
   uint64_t seed;
   int widths[BMLP_MAX_LAYERS + 1];
@@ -90,6 +90,7 @@ struct FwdArgs {
   const int32_t *y; int c;          // kFwdFusedSelect: labels [M] and class count
   const uint64_t *P; int ldp;       // kFwdFusedSelect: P_l rows [c][ldp], rho^{y^mu} = P_l[y^mu]
   int16_t *z; int ldz;              // kFwdWriteZ
+  float zlo, zhi;                   // kFwdFusedSelect: the selection clips z to [zlo, zhi]
   int32_t *zero; int nzero;         // if set: zeroed by the first work-group (step statistics)
   int nt_m, nt_n, xcd_remap;        // set by the launcher
   int pw_max, ystride;              // set by the launcher: last word of a P row; label stride
@@ -130,6 +131,7 @@ struct LossSelectArgs {
   uint8_t *err, *upd;
   int16_t *kstar; int ldk; // [groups][ldk]
   int32_t *stats;          // this layer's [4]
+  int zlo, zhi;            // the selection clips z to [zlo, zhi]
 };
 hipError_t launch_loss_select(const LossSelectArgs &a, hipStream_t s);
 

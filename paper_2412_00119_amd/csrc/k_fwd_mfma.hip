@@ -398,7 +398,8 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
 #pragma unroll
           for (int j = 0; j < 2; ++j) {
             const uint32_t r = (uint32_t)(rho >> (32 * j)) << sh;   // bit 31: rho of column j*32 + lc
-            const float sz = __uint_as_float(__float_as_uint(acc[i][j][e]) ^ (r & 0x80000000u));
+            const float zc = fminf(fmaxf(acc[i][j][e], p.zlo), p.zhi);   // z as the selection sees it
+            const float sz = __uint_as_float(__float_as_uint(zc) ^ (r & 0x80000000u));
             key[j] = __float_as_uint(sz - 0.5f) | (uint32_t)(j * 32 + lc);
           }
           v[i * 16 + e] = min(key[0], key[1]);

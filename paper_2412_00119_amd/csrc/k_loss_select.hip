@@ -88,7 +88,7 @@ __global__ __launch_bounds__(256) void loss_select_kernel(LossSelectArgs p) {
       const int k0 = g * p.gamma;
       for (int e = 0; e < p.gamma; ++e) {
         const int k = k0 + e;
-        const int zz = zr[k];
+        const int zz = min(max((int)zr[k], p.zlo), p.zhi);   // z as the selection sees it
         const bool rpos = (rho[k >> 6] >> (k & 63)) & 1ull;
         const bool wrong = rpos ? (zz < 0) : (zz > 0);
         const int a = zz < 0 ? -zz : zz;

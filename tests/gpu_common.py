@@ -40,12 +40,16 @@ def pack_np(pm1: np.ndarray, words: int) -> np.ndarray:
 class Pair:
     """A GPU network and an oracle network from the same configuration."""
 
-    def __init__(self, widths, c, bound, max_batch, gamma=64, r=0.25, seed=1, fwd_impl=0):
+    def __init__(self, widths, c, bound, max_batch, gamma=64, r=0.25, seed=1, fwd_impl=0, variants=0):
         torch = torch_cuda()
-        from paper_2412_00119_amd.bmlp import BMLP
+        from paper_2412_00119_amd import bmlp as B
         self.torch = torch
-        self.gpu = BMLP(widths, c, bound, max_batch, gamma, r, seed, fwd_impl)
-        self.ora = ob.init(ob.Config(widths, c, bound, gamma, r, seed))
+        self.gpu = B.BMLP(widths, c, bound, max_batch, gamma, r, seed, fwd_impl, variants=variants)
+        self.ora = ob.init(ob.Config(
+            widths, c, bound, gamma, r, seed,
+            fan_in_reinforce=bool(variants & B.BMLP_VARIANT_FAN_IN_REINFORCE),
+            shared_classifier=bool(variants & B.BMLP_VARIANT_SHARED_CLASSIFIER),
+            saturate_z=bool(variants & B.BMLP_VARIANT_SATURATE_Z)))
         self.widths = tuple(widths)
         self.c = c
 

@@ -138,3 +138,15 @@ def test_h_planes_hold_offset_values(bound, planes):
 def test_epoch_rescale_matches_oracle(p_r, wrong, samples):
     # host arithmetic in IEEE double on both sides: equal to the last bit
     assert B.bmlp_epoch_rescale(p_r, wrong, samples) == ob.rescale(p_r, wrong, samples)
+
+
+def test_variants_validated_and_shared_classifier_held_once():
+    cfg = B.make_config((20, 16, 16, 16), 3, 7, 8, group_size=4)
+    shared = B.make_config((20, 16, 16, 16), 3, 7, 8, group_size=4, variants=B.BMLP_VARIANT_SHARED_CLASSIFIER)
+    assert 0 < B.bmlp_state_bytes(shared) < B.bmlp_state_bytes(cfg)
+    offs = {B.bmlp_describe(shared, l).off_p for l in (1, 2, 3)}
+    assert len(offs) == 1
+    # unequal widths cannot share a classifier; unknown variant bits are refused
+    assert B.bmlp_state_bytes(B.make_config((20, 16, 8), 3, 7, 8, group_size=4,
+                                            variants=B.BMLP_VARIANT_SHARED_CLASSIFIER)) == 0
+    assert B.bmlp_state_bytes(B.make_config((20, 16), 3, 7, 8, group_size=4, variants=8)) == 0

@@ -1,0 +1,50 @@
+"""GPU parity of the method variants (bmlp_config.variants) with the
+oracle, bit for bit, every step: K_{l-1} in the reinforcement probability,
+one classifier shared by every layer, and the selection on z held in
+min(8, ceil(log2(2 K_{l-1}))) bits."""
+import numpy as np
+import pytest
+
+import oracle.bmlp as ob
+from paper_2412_00119_amd import bmlp as B
+from paper_2412_00119_amd import synth
+
+from gpu_common import Pair, note
+
+pytestmark = pytest.mark.gpu
+
+IMPLS = {"popcount": 1, "mfma_fp4": 2}
+VARIANTS = {
+    "fan_in": B.BMLP_VARIANT_FAN_IN_REINFORCE,
+    "shared": B.BMLP_VARIANT_SHARED_CLASSIFIER,
+    "saturate": B.BMLP_VARIANT_SATURATE_Z,
+    "all": B.BMLP_VARIANT_FAN_IN_REINFORCE | B.BMLP_VARIANT_SHARED_CLASSIFIER | B.BMLP_VARIANT_SATURATE_Z,
+}
+
+
+def _run(widths, gamma, variants, impl, steps=6, p_r=0.5, r=0.25):
+    w = synth.TINY    # prototype data: rows align with prototypes, so |z| grows past 127
+    p = Pair(widths, w.n_classes, 15, w.batch, gamma, r, seed=17, fwd_impl=IMPLS[impl], variants=variants)
+    d = synth.make_split(w, "train", n=steps * w.batch)
+    zmax = 0
+    for t, (x, y) in enumerate(d.batches(w.batch)):
+        note(f"variants {variants} impl {impl} widths {widths} step {t}")
+        p.step(x, y, t, p_r, tag=f"step {t}")
+        zmax = max(zmax, max(int(np.abs(ob.preactivation(x, p.ora.W(1))).max()), 0))
+    return p, zmax
+
+
+@pytest.mark.parametrize("impl", list(IMPLS))
+@pytest.mark.parametrize("name", list(VARIANTS))
+def test_variant_matches_oracle(name, impl):
+    p, zmax = _run((784, 256, 256), 64, VARIANTS[name], impl)
+    if name in ("saturate", "all"):
+        assert zmax > 128      # the clip to [-128, 127] was in play
+    if name in ("shared", "all"):
+        np.testing.assert_array_equal(p.gpu.P(1).cpu().numpy(), p.gpu.P(2).cpu().numpy())
+
+
+@pytest.mark.parametrize("impl", list(IMPLS))
+def test_saturated_selection_with_gamma_star(impl):
+    # gamma* = 105 for 525: the generic selection kernel reads z back
+    _run((784, 525), 0, B.BMLP_VARIANT_SATURATE_Z, impl, steps=4)
