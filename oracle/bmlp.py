@@ -51,6 +51,14 @@ project's design notes):
       exits at the first layer whose local classifier has a margin tau of
       at least ceil(r * K_l), the training-time robustness test, and at the
       last layer otherwise; its prediction is that layer's.
+  R18 median binarisation (Algorithm 1 line 5): each input feature is
+      compared with its median over a reference set of integer samples,
+      the lower middle order statistic (index floor((N-1)/2) of the sorted
+      column); +1 where x >= median.
+  R19 the expansion layer for integer inputs (Section 3.2, footnote 1):
+      a_0 = sign(x R^T) with R = ±1 [K_0][K_raw] fixed, exact integer sums,
+      sign(0) = +1; R from Philox stream 5 with layer word 2^32 - 1 and
+      t = 0, element j*K_raw + i at bit (e & 127) of block e >> 7.
 
 Random numbers come from Philox4x32-10 (``oracle.philox``) keyed by the
 64-bit seed (k0 = low word, k1 = high word), with counter
@@ -80,6 +88,7 @@ STREAM_H_INIT = 1
 STREAM_P_INIT = 2
 STREAM_R_COARSE = 3
 STREAM_R_FINE = 4
+STREAM_EXPAND = 5     # the fixed random input expansion layer (counter layer word 2^32 - 1)
 
 GAMMA_RANGE = (75, 105)   # the paper's empirical optimum range (Section 4.3)
 TWO32 = 1 << 32
@@ -309,6 +318,34 @@ def local_error(yhat: np.ndarray, y: np.ndarray, thr: int):
     err = pred != y
     upd = err | (tau < thr)
     return pred, tau, err, upd
+
+
+def feature_median(x: np.ndarray) -> np.ndarray:
+    """Per-feature median of integer samples x [N][K] (R18): the order
+    statistic floor((N-1)/2) of each column."""
+    x = np.asarray(x)
+    return np.sort(x, axis=0)[(len(x) - 1) // 2]
+
+
+def median_binarize(x: np.ndarray, median: np.ndarray) -> np.ndarray:
+    """Algorithm 1 line 5 (R18): +1 where a feature is at or above its median."""
+    return np.where(np.asarray(x) >= np.asarray(median)[None, :], 1, -1).astype(np.int8)
+
+
+def expansion_matrix(seed: int, k_raw: int, k0: int) -> np.ndarray:
+    """The fixed ±1 expansion weights R [K_0][K_raw] (R19)."""
+    k0s, k1s = philox_key(seed)
+    n = k_raw * k0
+    nb = (n + 127) // 128
+    words = np.stack(philox4x32_10(np.arange(nb, dtype=np.uint64), MASK32, 0, STREAM_EXPAND, k0s, k1s),
+                     axis=-1).astype("<u4")
+    bits = np.unpackbits(words.view(np.uint8).reshape(-1), bitorder="little")[:n]
+    return np.where(bits == 1, 1, -1).astype(np.int8).reshape(k0, k_raw)
+
+
+def expand(x: np.ndarray, R: np.ndarray) -> np.ndarray:
+    """Input layer for integer inputs (R19): a_0 = sign(x R^T), sign(0) = +1."""
+    return activation(int_matmul(np.asarray(x, dtype=np.int64), R.T))
 
 
 def z_bits(k_in: int) -> int:
