@@ -82,6 +82,7 @@ enum {
 #define BMLP_MAX_CLASSES 32767
 #define BMLP_MAX_GROUP 4096       /* gamma, bounded by on-chip bucket storage  */
 #define BMLP_MAX_BATCH 16384      /* pattern indices are kept in 15 bits on chip */
+#define BMLP_MAX_EXPAND_INPUTS 65536   /* |sum| <= 128 K_raw stays far inside int32 */
 
 /*
  * Network and hyper-parameters (Algorithm 1's variables and hyper-parameters;
@@ -194,6 +195,28 @@ int bmlp_attach(const bmlp_config *cfg, void *d_state, void *d_workspace, void *
  * rows [n][ceil(K/64)] (the step before the forward, Algorithm 1: the input
  * is already binarised).  n >= 0, K >= 1. */
 int bmlp_pack(const int8_t *d_pm1, int32_t n, int32_t K, uint64_t *d_bits, void *stream);
+
+/* The input side for integer features (Algorithm 1 line 5; Section 3.2,
+ * footnote 1).  Inputs are int8 rows [n][K], row-major; outputs are bit rows
+ * as bmlp_pack's (bit = 1 <=> +1, tail bits 0).  No context is needed.
+ *
+ * bmlp_feature_median: d_median int8 [K] receives each feature's median
+ * over the n >= 1 rows, the lower middle order statistic (element
+ * floor((n-1)/2) of the sorted column), so the threshold is one of the
+ * feature's values.
+ * bmlp_binarize: median binarisation, bit = (x >= d_median[feature]).
+ * 0 <= n <= 65535.
+ * bmlp_expand: the fixed random ±1 expansion layer for integer inputs,
+ * a_0[j] = sign(sum_i x_i R[j][i]) with sign(0) = +1, summed exactly in
+ * int32; R [k0][k_raw] is fixed by seed: element e = j k_raw + i is +1 iff
+ * bit (e & 127) of Philox4x32-10 block e >> 7 is set, counter (block,
+ * 2^32 - 1, 0, 5), key = seed.  d_bits [n][words(k0)];
+ * 1 <= k_raw <= BMLP_MAX_EXPAND_INPUTS, 1 <= k0 <= BMLP_MAX_WIDTH. */
+int bmlp_feature_median(const int8_t *d_x, int32_t n, int32_t K, int8_t *d_median, void *stream);
+int bmlp_binarize(const int8_t *d_x, int32_t n, int32_t K, const int8_t *d_median, uint64_t *d_bits,
+                  void *stream);
+int bmlp_expand(const int8_t *d_x, int32_t n, int32_t k_raw, int32_t k0, uint64_t seed, uint64_t *d_bits,
+                void *stream);
 
 /* Inference (Algorithm 1 forward and local outputs only): writes the local
  * output y_hat_l of every layer to d_yhat, int32 [L][n][n_classes].

@@ -93,6 +93,9 @@ def lib() -> ctypes.CDLL:
             "bmlp_train_step": (ctypes.c_int, [vp, vp, vp, i32, u64, dbl, vp, vp]),
             "bmlp_eval": (ctypes.c_int, [vp, vp, vp, i32, vp, vp]),
             "bmlp_eval_exit": (ctypes.c_int, [vp, vp, vp, i32, vp, vp]),
+            "bmlp_feature_median": (ctypes.c_int, [vp, i32, i32, vp, vp]),
+            "bmlp_binarize": (ctypes.c_int, [vp, i32, i32, vp, vp, vp]),
+            "bmlp_expand": (ctypes.c_int, [vp, i32, i32, i32, u64, vp, vp]),
             "bmlp_train_epoch": (ctypes.c_int, [vp, vp, vp, i32, vp, i32, i32, u64, dbl, vp, vp]),
             "bmlp_epoch_rescale": (dbl, [dbl, ctypes.c_int64, ctypes.c_int64]),
             "bmlp_layer_views": (ctypes.c_int, [vp, i32, ctypes.POINTER(vp), ctypes.POINTER(vp),
@@ -189,6 +192,47 @@ def bmlp_train_step(ctx: int, d_x: int, d_y: int, n: int, step: int, p_r: float,
 
 def bmlp_eval(ctx: int, d_x: int, d_y: int, n: int, d_correct: int, stream: int):
     _check(lib().bmlp_eval(ctx, d_x, d_y, n, d_correct, stream), "bmlp_eval")
+
+
+def bmlp_feature_median(d_x: int, n: int, K: int, d_median: int, stream: int):
+    _check(lib().bmlp_feature_median(d_x, n, K, d_median, stream), "bmlp_feature_median")
+
+
+def bmlp_binarize(d_x: int, n: int, K: int, d_median: int, d_bits: int, stream: int):
+    _check(lib().bmlp_binarize(d_x, n, K, d_median, d_bits, stream), "bmlp_binarize")
+
+
+def bmlp_expand(d_x: int, n: int, k_raw: int, k0: int, seed: int, d_bits: int, stream: int):
+    _check(lib().bmlp_expand(d_x, n, k_raw, k0, seed & (2**64 - 1), d_bits, stream), "bmlp_expand")
+
+
+def feature_median(x_int8):
+    """Per-feature lower median of int8 rows [n][K] (a CUDA tensor), int8 [K]."""
+    import torch
+    n, K = x_int8.shape
+    out = torch.empty(K, dtype=torch.int8, device=x_int8.device)
+    bmlp_feature_median(x_int8.data_ptr(), n, K, out.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    return out
+
+
+def binarize(x_int8, median):
+    """Median binarisation of int8 rows [n][K] to bit rows int64 [n][ceil(K/64)]."""
+    import torch
+    n, K = x_int8.shape
+    out = torch.empty((n, words64(K)), dtype=torch.int64, device=x_int8.device)
+    bmlp_binarize(x_int8.data_ptr(), n, K, median.data_ptr(), out.data_ptr(),
+                  torch.cuda.current_stream().cuda_stream)
+    return out
+
+
+def expand(x_int8, k0: int, seed: int):
+    """The fixed random ±1 expansion layer: int8 rows [n][K_raw] to bit rows
+    int64 [n][ceil(k0/64)]."""
+    import torch
+    n, k_raw = x_int8.shape
+    out = torch.empty((n, words64(k0)), dtype=torch.int64, device=x_int8.device)
+    bmlp_expand(x_int8.data_ptr(), n, k_raw, k0, int(seed), out.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    return out
 
 
 def bmlp_eval_exit(ctx: int, d_x: int, d_y: int, n: int, d_counts: int, stream: int):

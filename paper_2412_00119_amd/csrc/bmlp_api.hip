@@ -383,6 +383,29 @@ int bmlp_pack(const int8_t *d_pm1, int32_t n, int32_t K, uint64_t *d_bits, void 
   return BMLP_OK;
 }
 
+int bmlp_feature_median(const int8_t *d_x, int32_t n, int32_t K, int8_t *d_median, void *stream) {
+  if (n < 1 || K < 1) return BMLP_ESHAPE;
+  if (d_x == nullptr || d_median == nullptr) return BMLP_EINVAL;
+  BMLP_LAUNCH(launch_feature_median(d_x, n, K, d_median, as_stream(stream)));
+  return BMLP_OK;
+}
+
+int bmlp_binarize(const int8_t *d_x, int32_t n, int32_t K, const int8_t *d_median, uint64_t *d_bits,
+                  void *stream) {
+  if (n < 0 || K < 1 || n > 65535) return BMLP_ESHAPE;
+  if (n > 0 && (d_x == nullptr || d_median == nullptr || d_bits == nullptr)) return BMLP_EINVAL;
+  BMLP_LAUNCH(launch_binarize(d_x, n, K, d_median, d_bits, as_stream(stream)));
+  return BMLP_OK;
+}
+
+int bmlp_expand(const int8_t *d_x, int32_t n, int32_t k_raw, int32_t k0, uint64_t seed, uint64_t *d_bits,
+                void *stream) {
+  if (n < 0 || k_raw < 1 || k_raw > BMLP_MAX_EXPAND_INPUTS || k0 < 1 || k0 > BMLP_MAX_WIDTH) return BMLP_ESHAPE;
+  if (n > 0 && (d_x == nullptr || d_bits == nullptr)) return BMLP_EINVAL;
+  BMLP_LAUNCH(launch_expand(d_x, n, k_raw, k0, seed, d_bits, as_stream(stream)));
+  return BMLP_OK;
+}
+
 int bmlp_forward(bmlp_ctx *ctx, const uint64_t *d_x, int32_t n, int32_t *d_yhat, void *stream) {
   int st = check_ctx_batch(ctx, d_x, n);
   if (st != BMLP_OK) return st;

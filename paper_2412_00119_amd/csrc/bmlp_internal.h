@@ -148,6 +148,12 @@ hipError_t launch_exit_count(const uint8_t *flags, int ldf, int L, int n, int32_
 hipError_t launch_gather_batch(const uint64_t *x_all, const int32_t *y_all, int n_all, int words,
                                const int32_t *order, int n, uint64_t *xb, int32_t *yb, hipStream_t s);
 
+// The input side (int8 features): per-feature lower median over n rows;
+// bit = (x >= thr) rows; the fixed random ±1 expansion layer sign(x R^T).
+hipError_t launch_feature_median(const int8_t *x, int n, int K, int8_t *med, hipStream_t s);
+hipError_t launch_binarize(const int8_t *x, int n, int K, const int8_t *thr, uint64_t *bits, hipStream_t s);
+hipError_t launch_expand(const int8_t *x, int n, int k_raw, int k0, uint64_t seed, uint64_t *bits, hipStream_t s);
+
 // Clipped-Perceptron increments + reinforcement + clip + re-sign of up to
 // kMaxUpdLayers layers in one launch.
 struct UpdLayer {

@@ -150,3 +150,11 @@ def test_variants_validated_and_shared_classifier_held_once():
     assert B.bmlp_state_bytes(B.make_config((20, 16, 8), 3, 7, 8, group_size=4,
                                             variants=B.BMLP_VARIANT_SHARED_CLASSIFIER)) == 0
     assert B.bmlp_state_bytes(B.make_config((20, 16), 3, 7, 8, group_size=4, variants=8)) == 0
+
+
+def test_input_side_shapes_rejected_before_any_launch():
+    assert B.lib().bmlp_expand(None, 4, 0, 64, 1, None, None) == B.BMLP_ESHAPE
+    assert B.lib().bmlp_expand(None, 4, 10, 0, 1, None, None) == B.BMLP_ESHAPE
+    assert B.lib().bmlp_expand(None, 4, 10, 64, 1, None, None) == B.BMLP_EINVAL
+    assert B.lib().bmlp_feature_median(None, 0, 8, None, None) == B.BMLP_ESHAPE
+    assert B.lib().bmlp_binarize(None, 3, 8, None, None, None) == B.BMLP_EINVAL
