@@ -196,7 +196,7 @@ int bmlp_attach(const bmlp_config *cfg, void *d_state, void *d_workspace, void *
  * is already binarised).  n >= 0, K >= 1. */
 int bmlp_pack(const int8_t *d_pm1, int32_t n, int32_t K, uint64_t *d_bits, void *stream);
 
-/* The input side for integer features (Algorithm 1 line 5; Section 3.2,
+/* The input side for integer features (Algorithm 1, its binarisation of the inputs; Section 3.2,
  * footnote 1).  Inputs are int8 rows [n][K], row-major; outputs are bit rows
  * as bmlp_pack's (bit = 1 <=> +1, tail bits 0).  No context is needed.
  *
@@ -259,7 +259,7 @@ int bmlp_eval(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int32_t n,
 int bmlp_eval_exit(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int32_t n,
                    int32_t *d_counts, void *stream);
 
-/* One epoch of Algorithm 1 (its epoch loop, lines 3-20) over a training set
+/* One epoch of Algorithm 1 (its loop over mini-batches) over a training set
  * resident on the device: d_x_all bit rows [n_all][words(K_0)], d_y_all
  * int32 [n_all].  d_order int32 [n_order] lists training-set indices (the
  * caller's shuffle; indices outside [0, n_all) are clamped into range).
@@ -277,7 +277,7 @@ int bmlp_train_epoch(bmlp_ctx *ctx, const uint64_t *d_x_all, const int32_t *d_y_
                      const int32_t *d_order, int32_t n_order, int32_t batch, uint64_t step0, double p_r,
                      int32_t *d_stats, void *stream);
 
-/* The rescale at the end of an epoch (Algorithm 1 line 21, Section 3.4):
+/* The rescale at the end of an epoch (Algorithm 1, the end of its epoch loop; Section 3.4):
  * p_r * sqrt(wrong / samples) in IEEE double, or p_r unchanged when no
  * sample was trained on.  Host only. */
 double bmlp_epoch_rescale(double p_r, int64_t wrong, int64_t samples);

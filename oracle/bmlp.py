@@ -51,7 +51,7 @@ project's design notes):
       exits at the first layer whose local classifier has a margin tau of
       at least ceil(r * K_l), the training-time robustness test, and at the
       last layer otherwise; its prediction is that layer's.
-  R18 median binarisation (Algorithm 1 line 5): each input feature is
+  R18 median binarisation (Algorithm 1, its input step): each input feature is
       compared with its median over a reference set of integer samples,
       the lower middle order statistic (index floor((N-1)/2) of the sorted
       column); +1 where x >= median.
@@ -59,6 +59,12 @@ project's design notes):
       a_0 = sign(x R^T) with R = ±1 [K_0][K_raw] fixed, exact integer sums,
       sign(0) = +1; R from Philox stream 5 with layer word 2^32 - 1 and
       t = 0, element j*K_raw + i at bit (e & 127) of block e >> 7.
+  R20 group reshuffle (Section 4.3 varies group membership without giving
+      the draw): at step t layer l orders its perceptrons by the 32-bit
+      key word (k & 3) of Philox block k >> 2, stream 6, ties by index, and
+      group g is positions g*gamma .. g*gamma + gamma - 1 of that order;
+      k* is stored as the position within the group, and equal deltas go
+      to the lowest perceptron index, as with fixed groups.
 
 Random numbers come from Philox4x32-10 (``oracle.philox``) keyed by the
 64-bit seed (k0 = low word, k1 = high word), with counter
@@ -71,6 +77,9 @@ Random numbers come from Philox4x32-10 (``oracle.philox``) keyed by the
             bit p of u8 is bit (i & 31) of word p & 3 of block 2q + (p >> 2).
   stream 4  reinforcement, fine bits: u24 = low 24 bits of word (j & 3) of
             block j >> 2, j = k * K_{l-1} + i.
+  stream 5  expansion layer (R19).
+  stream 6  group order (R20): key of perceptron k is word (k & 3) of
+            block k >> 2.
   The 32-bit draw of hidden weight (k, i) is u = u8 * 2^24 + u24; it
   reinforces when u < T_l.  Init uses t = 0.
 """
@@ -89,6 +98,7 @@ STREAM_P_INIT = 2
 STREAM_R_COARSE = 3
 STREAM_R_FINE = 4
 STREAM_EXPAND = 5     # the fixed random input expansion layer (counter layer word 2^32 - 1)
+STREAM_GROUPS = 6     # per-step group membership (reshuffle variant)
 
 GAMMA_RANGE = (75, 105)   # the paper's empirical optimum range (Section 4.3)
 TWO32 = 1 << 32
@@ -222,6 +232,7 @@ class Config:
     fan_in_reinforce: bool = False   # K_{l-1} instead of K_l in the reinforcement probability
     shared_classifier: bool = False  # one P for every layer (all K_l equal, Section 3.1)
     saturate_z: bool = False         # z held in min(8, ceil(log2(2 K_{l-1}))) bits (Section 3.5)
+    reshuffle_groups: bool = False   # random group membership every step (Section 4.3)
 
     def __post_init__(self):
         self.widths = tuple(int(v) for v in self.widths)
@@ -328,7 +339,7 @@ def feature_median(x: np.ndarray) -> np.ndarray:
 
 
 def median_binarize(x: np.ndarray, median: np.ndarray) -> np.ndarray:
-    """Algorithm 1 line 5 (R18): +1 where a feature is at or above its median."""
+    """Algorithm 1's input binarisation (R18): +1 where a feature is at or above its median."""
     return np.where(np.asarray(x) >= np.asarray(median)[None, :], 1, -1).astype(np.int8)
 
 
@@ -361,28 +372,45 @@ def saturate(z: np.ndarray, k_in: int) -> np.ndarray:
     return np.clip(z, -(1 << (b - 1)), (1 << (b - 1)) - 1)
 
 
-def select_easiest(z: np.ndarray, P: np.ndarray, y: np.ndarray, upd: np.ndarray, gamma: int) -> np.ndarray:
-    """Algorithm 2: for each pattern in M and each group of gamma contiguous
-    perceptrons, the index (within the group) of the largest negative
-    stability delta = z * rho^{y}; -1 where the pattern is not in M or the
-    group has no negative stability.  Ties take the lowest index (R5, R6)."""
+def group_permutation(seed: int, layer: int, t: int, k: int) -> np.ndarray:
+    """The reshuffle variant's group order at step t: perceptrons sorted by
+    a 32-bit Philox key (word k & 3 of block k >> 2 of stream 6, counter
+    (block, l-1, t, 6)), ties by index; group g holds positions
+    g*gamma .. g*gamma + gamma - 1 of this order."""
+    idx = np.arange(k)
+    words, _ = _blocks(seed, layer, t, STREAM_GROUPS, np.arange((k + 3) // 4, dtype=np.uint64))
+    return np.lexsort((idx, words[idx >> 2, idx & 3]))
+
+
+def select_easiest(z: np.ndarray, P: np.ndarray, y: np.ndarray, upd: np.ndarray, gamma: int,
+                   perm: Optional[np.ndarray] = None) -> np.ndarray:
+    """Algorithm 2: for each pattern in M and each group of gamma perceptrons
+    (contiguous, or positions of ``perm`` in the reshuffle variant), the
+    offset within the group of the largest negative stability
+    delta = z * rho^{y}; -1 where the pattern is not in M or the group has
+    no negative stability.  Ties take the lowest perceptron index (R5, R6)."""
     n, k = z.shape
     g = k // gamma
     rho = P[y].astype(np.int64)                     # [n][K_l], rho^{y^mu}
-    delta = (z * rho).reshape(n, g, gamma)
+    order = np.arange(k) if perm is None else np.asarray(perm, dtype=np.int64)
+    delta = (z * rho)[:, order].reshape(n, g, gamma)
     neg = delta < 0
-    key = np.where(neg, delta, np.iinfo(np.int64).min)
-    kstar = np.argmax(key, axis=2)                   # first index of the max
+    # the largest delta, then the lowest perceptron index (0 <= index < K_l)
+    comp = delta * k - order.reshape(1, g, gamma)
+    key = np.where(neg, comp, np.iinfo(np.int64).min)
+    kstar = np.argmax(key, axis=2)
     ok = neg.any(axis=2) & upd[:, None]
     return np.where(ok, kstar, -1).astype(np.int16)
 
 
-def selection_matrix(kstar: np.ndarray, P: np.ndarray, y: np.ndarray, gamma: int) -> np.ndarray:
+def selection_matrix(kstar: np.ndarray, P: np.ndarray, y: np.ndarray, gamma: int,
+                     perm: Optional[np.ndarray] = None) -> np.ndarray:
     """S[mu][k] = rho^{y^mu, k} for every selected pair (mu, k) of U_l, else 0."""
     n, g = kstar.shape
     S = np.zeros((n, g * gamma), dtype=np.int8)
     mu, grp = np.nonzero(kstar >= 0)
-    k = grp * gamma + kstar[mu, grp].astype(np.int64)
+    pos = grp * gamma + kstar[mu, grp].astype(np.int64)
+    k = pos if perm is None else np.asarray(perm, dtype=np.int64)[pos]
     S[mu, k] = P[y[mu], k]
     return S
 
@@ -413,6 +441,7 @@ class LayerTrace:
     upd: np.ndarray       # bool [n]
     kstar: np.ndarray     # int16 [n][G]
     stats: np.ndarray     # int64 [4]: sum(err), |M|, |U|, reinforced draws
+    perm: Optional[np.ndarray] = None   # the step's group order (reshuffle variant)
 
 
 def train_step(state: State, x: np.ndarray, y: np.ndarray, t: int, p_r: float,
@@ -441,19 +470,20 @@ def train_step(state: State, x: np.ndarray, y: np.ndarray, t: int, p_r: float,
             z = saturate(z, kin)
         yhat = local_output(a, P)
         pred, tau, err, upd = local_error(yhat, y, robustness_threshold(cfg.robustness, kout))
-        kstar = select_easiest(z, P, y, upd, gamma)
+        perm = group_permutation(cfg.seed, l, t, kout) if cfg.reshuffle_groups else None
+        kstar = select_easiest(z, P, y, upd, gamma, perm)
         nsel = int((kstar >= 0).sum())
         nreinf = 0
         if l in want and upd.any():
             # LayerUpdate / PerceptronUpdate run only when M_l is not empty.
-            S = selection_matrix(kstar, P, y, gamma)
+            S = selection_matrix(kstar, P, y, gamma, perm)
             h1 = clip(H.astype(np.int64) + cp_increment(S, a_prev), cfg.bound)
             kq = kin if cfg.fan_in_reinforce else kout     # R11, or the fan-in variant
             mask = reinforce_mask(cfg.seed, l, t, reinforce_threshold(p_r, kq), kin * kout, kin)
             nreinf = int(mask.sum())
             state.H[l - 1] = reinforce(h1, mask, cfg.bound).astype(np.int8)
         traces.append(LayerTrace(a, z, yhat, pred, tau, err, upd, kstar,
-                                 np.array([err.sum(), upd.sum(), nsel, nreinf], dtype=np.int64)))
+                                 np.array([err.sum(), upd.sum(), nsel, nreinf], dtype=np.int64), perm))
         a_prev = a
     return traces
 
@@ -469,7 +499,7 @@ def forward(state: State, x: np.ndarray) -> List[np.ndarray]:
 
 
 def rescale(p_r: float, wrong: int, samples: int) -> float:
-    """p_r * sqrt(E^e) with E^e = wrong / samples (Algorithm 1 line 21,
+    """p_r * sqrt(E^e) with E^e = wrong / samples (the end of Algorithm 1's epoch loop,
     Section 3.4); unchanged when no sample was trained on (R16)."""
     if samples <= 0:
         return p_r
@@ -486,8 +516,8 @@ class EpochResult:
 
 def train_epoch(state: State, x: np.ndarray, y: np.ndarray, order: np.ndarray, batch: int,
                 t0: int, p_r: float) -> EpochResult:
-    """One pass of Algorithm 1's epoch loop (its lines 4-20) and the rescale of
-    line 21 (Section 3.4), R16: the full batches order[b*batch:(b+1)*batch]
+    """One pass of Algorithm 1's loop over mini-batches and the rescale that
+    ends the epoch (Section 3.4), R16: the full batches order[b*batch:(b+1)*batch]
     of the training set x (int8 ±1 [N][K_0]), y, trained with steps t0 + b,
     all at the given p_r."""
     order = np.asarray(order, dtype=np.int64)

@@ -486,7 +486,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
     ls.zlo = zlo; ls.zhi = zhi;
     if (mfma) {
       const bool fused = lp.gamma == 64;
-      // Algorithm 1 lines 8-9, and Algorithm 2's choice when fused
+      // Algorithm 1's pre-activation and sign, and Algorithm 2's choice when fused
       FwdArgs f{};
       f.A = a_prev; f.lda = lp.words_in;
       f.B = W; f.ldb = lp.words_in;
@@ -517,7 +517,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
     a_prev = a;
   }
   if (mfma) {
-    // Algorithm 1 lines 10-15 for every layer, one launch per kMaxClsLayers layers
+    // Algorithm 1's local output, loss and robustness test for every layer, one launch per kMaxClsLayers layers
     ClsBatch cb{};
     cb.n = n; cb.c = p.c; cb.y = d_y; cb.mode = kClsTrain;
     for (int l = 1; l <= p.L; ++l) {

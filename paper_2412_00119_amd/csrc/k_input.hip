@@ -1,4 +1,4 @@
-// The input side of the step (Algorithm 1 line 5 and Section 3.2,
+// The input side of the step (Algorithm 1's binarisation of the inputs and Section 3.2,
 // footnote 1), for integer features (int8):
 //   * the median of every feature over a reference set (the lower middle
 //     order statistic, so an element of the column and exact);

@@ -58,7 +58,7 @@ def brute_layer(a_prev, W, P, y, thr, gamma):
 
 
 def brute_cp(H, a_prev, P, y, kstar, gamma, bound):
-    """Algorithm 3 lines 2-4 applied one selected pair at a time, no clipping
+    """Algorithm 3's clipped-perceptron increment applied one selected pair at a time, no clipping
     inside the loop, clip once at the end."""
     h = [[int(v) for v in row] for row in H]
     n, G = kstar.shape

@@ -1,4 +1,4 @@
-"""Pins the oracle's input side: median binarisation (Algorithm 1 line 5,
+"""Pins the oracle's input side: median binarisation (Algorithm 1's input step,
 reading R18) and the fixed random ±1 expansion layer for integer inputs
 (Section 3.2, footnote 1; reading R19)."""
 import numpy as np

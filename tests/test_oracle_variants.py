@@ -86,3 +86,86 @@ def test_saturated_selection_brute_force():
         np.testing.assert_array_equal(tr.kstar, _brute_select(zs, st.P[0][y], tr.upd, 16))
         picks.append(tr.kstar)
     assert not np.array_equal(picks[0], picks[1])   # saturation changed a choice
+
+
+def test_group_permutation_layout():
+    # the key of perceptron k is word k & 3 of Philox block k >> 2 of stream
+    # 6 at counter (block, l-1, t, 6); the order sorts keys, ties by index
+    from oracle.philox import philox4x32_10
+    seed, layer, t, k = 11, 2, 5, 37
+    k0, k1 = ob.philox_key(seed)
+    keys = []
+    for kk in range(k):
+        w = philox4x32_10(np.array([kk >> 2], np.uint64), layer - 1, t, 6, k0, k1)
+        keys.append(int(w[kk & 3][0]))
+    want = sorted(range(k), key=lambda i: (keys[i], i))
+    got = ob.group_permutation(seed, layer, t, k)
+    assert sorted(got.tolist()) == list(range(k))
+    assert got.tolist() == want
+    assert ob.group_permutation(seed, layer, t + 1, k).tolist() != want
+
+
+def _brute_select_perm(z, rho_rows, upd, gamma, perm):
+    n, k = z.shape
+    out = -np.ones((n, k // gamma), dtype=np.int64)
+    for mu in range(n):
+        if not upd[mu]:
+            continue
+        for g in range(k // gamma):
+            best, bkey = -1, None
+            for e in range(gamma):
+                kk = int(perm[g * gamma + e])
+                d = int(z[mu, kk]) * int(rho_rows[mu][kk])
+                key = (abs(int(z[mu, kk])), kk)
+                if d < 0 and (bkey is None or key < bkey):
+                    best, bkey = e, key
+            out[mu, g] = best
+    return out
+
+
+def test_reshuffled_selection_brute_force():
+    # small K_{l-1} makes many |z| ties, so the lowest-index rule is exercised
+    cfg = ob.Config((6, 32, 16), 3, 7, 4, 100.0, seed=9, reshuffle_groups=True)
+    st = ob.init(cfg)
+    rng = np.random.default_rng(4)
+    x, y = random_pm1((40, 6), rng), rng.integers(0, 3, 40)
+    for t in range(3):
+        before = st.copy()
+        tr = ob.train_step(st, x, y, t, 0.0)
+        for l, lt in enumerate(tr, start=1):
+            perm = ob.group_permutation(cfg.seed, l, t, cfg.widths[l])
+            np.testing.assert_array_equal(lt.perm, perm)
+            np.testing.assert_array_equal(
+                lt.kstar, _brute_select_perm(lt.z, before.P[l - 1][y], lt.upd, 4, perm))
+            # the clipped-perceptron step moves exactly the selected rows
+            S = ob.selection_matrix(lt.kstar, before.P[l - 1], y, 4, perm)
+            moved = np.nonzero((st.H[l - 1] != before.H[l - 1]).any(axis=1))[0]
+            assert set(moved.tolist()) <= set(np.nonzero(S.any(axis=0))[0].tolist())
+
+
+def test_reshuffle_one_group_is_fixed_groups():
+    # with gamma = K_l there is one group whatever the order, so training
+    # is the same as with fixed groups
+    runs = []
+    for rs in (False, True):
+        cfg = ob.Config((24, 16, 16), 2, 7, 16, 0.5, seed=13, reshuffle_groups=rs)
+        st = ob.init(cfg)
+        rng = np.random.default_rng(6)
+        for t in range(4):
+            ob.train_step(st, random_pm1((32, 24), rng), rng.integers(0, 2, 32), t, 0.3)
+        runs.append(st)
+    for a, b in zip(runs[0].H, runs[1].H):
+        np.testing.assert_array_equal(a, b)
+
+
+def test_reshuffle_changes_groups():
+    cfg = ob.Config((24, 32), 2, 7, 4, 100.0, seed=13, reshuffle_groups=True)
+    fixed = ob.Config((24, 32), 2, 7, 4, 100.0, seed=13)
+    rng = np.random.default_rng(8)
+    x, y = random_pm1((32, 24), rng), rng.integers(0, 2, 32)
+    S = []
+    for c in (cfg, fixed):
+        st = ob.init(c)
+        tr = ob.train_step(st.copy(), x, y, 0, 0.0)[0]
+        S.append(ob.selection_matrix(tr.kstar, st.P[0], y, 4, tr.perm))
+    assert not np.array_equal(S[0], S[1])
