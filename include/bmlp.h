@@ -74,6 +74,13 @@ enum {
    * bits, i.e. clipped to [-2^(b-1), 2^(b-1) - 1] (Section 3.5); a_l keeps
    * the sign of the exact z. */
   BMLP_VARIANT_SATURATE_Z = 4,
+  /* group membership drawn again every step (Section 4.3): layer l orders
+   * its K_l perceptrons by a 32-bit key, word (k & 3) of Philox block
+   * k >> 2 of stream 6 at counter (block, l - 1, t, 6), ties by index, and
+   * group g is positions g*gamma .. g*gamma + gamma - 1 of that order.  k*
+   * is then a position within the group; equal stabilities go to the
+   * lowest perceptron index. */
+  BMLP_VARIANT_RESHUFFLE_GROUPS = 8,
 };
 
 /* Limits of this build. */

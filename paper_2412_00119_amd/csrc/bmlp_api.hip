@@ -118,7 +118,8 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
       cfg->fwd_impl != BMLP_FWD_MFMA_FP4)
     return BMLP_EINVAL;
   constexpr int kAllVariants =
-      BMLP_VARIANT_FAN_IN_REINFORCE | BMLP_VARIANT_SHARED_CLASSIFIER | BMLP_VARIANT_SATURATE_Z;
+      BMLP_VARIANT_FAN_IN_REINFORCE | BMLP_VARIANT_SHARED_CLASSIFIER | BMLP_VARIANT_SATURATE_Z |
+      BMLP_VARIANT_RESHUFFLE_GROUPS;
   if (cfg->variants & ~kAllVariants) return BMLP_EINVAL;
   memset(p, 0, sizeof(*p));
   p->variants = cfg->variants;
@@ -176,6 +177,8 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
     wo = align256(wo + (size_t)nb);
     lp.off_kstar = wo;
     wo = align256(wo + (size_t)nb * lp.groups * 2);
+    lp.off_perm = wo;
+    wo = align256(wo + (p->variants & BMLP_VARIANT_RESHUFFLE_GROUPS ? (size_t)lp.k_out * 4 : 0));
   }
   p->off_flag = wo;   // early-exit flags [L][max_batch]
   wo = align256(wo + (size_t)p->L * nb);
@@ -459,6 +462,21 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
   if (n == 0) return BMLP_OK;
   int16_t *z = reinterpret_cast<int16_t *>(ctx->ws + p.off_z);
   int32_t *yh = reinterpret_cast<int32_t *>(ctx->ws + p.off_yhat);
+  const bool reshuffle = p.variants & BMLP_VARIANT_RESHUFFLE_GROUPS;
+  if (reshuffle) {   // this step's group order of every layer
+    PermBatch pb{};
+    pb.key0 = (uint32_t)p.seed; pb.key1 = (uint32_t)(p.seed >> 32); pb.step = (uint32_t)step;
+    for (int l = 1; l <= p.L; ++l) {
+      PermLayer &q = pb.L[pb.nl++];
+      q.perm = reinterpret_cast<int32_t *>(ctx->ws + p.layer[l - 1].off_perm);
+      q.k = p.layer[l - 1].k_out;
+      q.ctr1 = (uint32_t)(l - 1);
+      if (pb.nl == 8 || l == p.L) {
+        BMLP_TIMED(ctx, BMLP_KERNEL_SELECT, s, launch_group_perm(pb, s));
+        pb.nl = 0;
+      }
+    }
+  }
   const uint64_t *a_prev = d_x;
   for (int l = 1; l <= p.L; ++l) {
     const LayerPlan &lp = p.layer[l - 1];
@@ -484,8 +502,11 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
       zhi = (1 << (b - 1)) - 1;
     }
     ls.zlo = zlo; ls.zhi = zhi;
+    const int32_t *perm = reshuffle ? reinterpret_cast<const int32_t *>(ctx->ws + lp.off_perm) : nullptr;
+    ls.perm = perm;
     if (mfma) {
-      const bool fused = lp.gamma == 64;
+      // the fused selection takes contiguous groups of 64
+      const bool fused = lp.gamma == 64 && !reshuffle;
       // Algorithm 1's pre-activation and sign, and Algorithm 2's choice when fused
       FwdArgs f{};
       f.A = a_prev; f.lda = lp.words_in;
@@ -557,6 +578,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
     const uint64_t T = reinforce_threshold(p_r, (p.variants & BMLP_VARIANT_FAN_IN_REINFORCE) ? lp.k_in : lp.k_out);
     u.t_hi = (uint32_t)(T >> 24); u.t_lo = (uint32_t)(T & 0xFFFFFFu);
     u.ctr1 = (uint32_t)(l - 1);
+    u.perm = reshuffle ? reinterpret_cast<const int32_t *>(ctx->ws + lp.off_perm) : nullptr;
     if (ub.nl == kMaxUpdLayers || l == p.L) {
       BMLP_TIMED(ctx, BMLP_KERNEL_UPDATE, s, launch_update(ub, s));
       ub.nl = 0;

@@ -15,6 +15,7 @@ enum : uint32_t {
   kStreamPInit = 2,     // P_l entries
   kStreamCoarse = 3,    // reinforcement: top byte of the 32-bit draw
   kStreamFine = 4,      // reinforcement: low 24 bits of the 32-bit draw
+  kStreamGroups = 6,    // per-step group order (reshuffle variant)
 };
 
 // Bit planes of H: u = (h + B) / 2 lies in [0, B], B odd.
@@ -31,7 +32,7 @@ struct LayerPlan {
   int h_ps;                  // 32-bit words per plane of an H row, multiple of 16
   int robust_thr;            // ceil(r K_l)
   size_t off_h, off_w, off_p;                              // state
-  size_t off_a, off_err, off_upd, off_kstar;               // workspace
+  size_t off_a, off_err, off_upd, off_kstar, off_perm;     // workspace
 };
 
 struct Plan {
@@ -132,6 +133,7 @@ struct LossSelectArgs {
   int16_t *kstar; int ldk; // [groups][ldk]
   int32_t *stats;          // this layer's [4]
   int zlo, zhi;            // the selection clips z to [zlo, zhi]
+  const int32_t *perm;     // group order [k_out] (reshuffle variant), or null: contiguous
 };
 hipError_t launch_loss_select(const LossSelectArgs &a, hipStream_t s);
 
@@ -168,6 +170,7 @@ struct UpdLayer {
   int chunks, block0;      // filled by launch_update
   uint32_t t_hi, t_lo;     // T_l >> 24 (0..256) and T_l & 0xFFFFFF
   uint32_t ctr1;           // layer - 1
+  const int32_t *perm;     // group order [k_out], or null: contiguous groups
 };
 constexpr int kMaxUpdLayers = 8;
 struct UpdateBatch {
@@ -178,5 +181,21 @@ struct UpdateBatch {
   uint32_t key0, key1, step;
 };
 hipError_t launch_update(UpdateBatch &b, hipStream_t s);
+
+// The reshuffle variant's group order of each layer at one step: perm[i]
+// is the perceptron at position i when the K perceptrons are sorted by
+// their stream-6 keys, ties by index.
+struct PermLayer {
+  int32_t *perm;
+  int k;
+  uint32_t ctr1;           // layer - 1
+  int block0;              // filled by launch_group_perm
+};
+struct PermBatch {
+  PermLayer L[8];
+  int nl;
+  uint32_t key0, key1, step;
+};
+hipError_t launch_group_perm(PermBatch &b, hipStream_t s);
 
 }  // namespace bmlp

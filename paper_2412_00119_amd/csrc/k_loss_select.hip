@@ -4,13 +4,15 @@
 // One wave per pattern.  Given y_hat, the wave finds the first argmax and the
 // two largest values (tau = top1 - top2, 0 on a tie), sets err = (pred != y)
 // and upd = err or tau < ceil(r K_l).  For every pattern it then takes, in
-// every group of gamma contiguous perceptrons, the one with the largest
+// every group of gamma perceptrons (contiguous, or consecutive in the
+// reshuffle variant's per-step order), the one with the largest
 // negative stability delta_k = z_k rho^{y}_k, i.e. the smallest |z_k| among
 // those whose sign disagrees with rho^{y}_k, lowest k on ties; delta = 0 is
 // not eligible.  The update keeps only the patterns in M.
 #include <limits.h>
 
 #include "bmlp_internal.h"
+#include "philox.h"
 
 namespace bmlp {
 namespace {
@@ -84,16 +86,17 @@ __global__ __launch_bounds__(256) void loss_select_kernel(LossSelectArgs p) {
     const int16_t *zr = p.z + (size_t)mu * p.ldz;
     const uint64_t *rho = p.P + (size_t)yl * p.words_out;
     for (int g = lane; g < p.groups; g += 64) {
-      int best = -1, bestabs = INT_MAX;
+      int best = -1, bestabs = INT_MAX, bestk = INT_MAX;
       const int k0 = g * p.gamma;
       for (int e = 0; e < p.gamma; ++e) {
-        const int k = k0 + e;
+        const int k = p.perm ? p.perm[k0 + e] : k0 + e;
         const int zz = min(max((int)zr[k], p.zlo), p.zhi);   // z as the selection sees it
         const bool rpos = (rho[k >> 6] >> (k & 63)) & 1ull;
         const bool wrong = rpos ? (zz < 0) : (zz > 0);
         const int a = zz < 0 ? -zz : zz;
-        if (wrong && a < bestabs) {
+        if (wrong && (a < bestabs || (a == bestabs && k < bestk))) {   // ties: lowest k
           bestabs = a;
+          bestk = k;
           best = e;
         }
       }
@@ -170,11 +173,75 @@ __global__ __launch_bounds__(256) void gather_batch_kernel(const uint64_t *x_all
   if (w == 0) yb[i] = y_all[src];
 }
 
+// The reshuffle variant's group order: perceptron k's key is word (k & 3)
+// of stream-6 block k >> 2, and its position is its rank among all K keys
+// (ties by index).  One thread per perceptron counts the keys below its
+// own, with the keys staged through LDS kPermChunk at a time; every block
+// makes each chunk's keys itself (a few Philox blocks per thread).
+constexpr int kPermThreads = 256;
+constexpr int kPermChunk = 2048;
+
+__device__ __forceinline__ uint32_t word_of(const U32x4 &w, int i) {
+  return i == 0 ? w.x : i == 1 ? w.y : i == 2 ? w.z : w.w;
+}
+
+__global__ __launch_bounds__(kPermThreads) void group_perm_kernel(PermBatch p) {
+  __shared__ uint4 keys[kPermChunk / 4];
+  int li = 0;
+#pragma unroll 1
+  for (int i = 1; i < p.nl; ++i)
+    if ((int)blockIdx.x >= p.L[i].block0) li = i;
+  const PermLayer &q = p.L[li];
+  const int k = ((int)blockIdx.x - q.block0) * kPermThreads + (int)threadIdx.x;
+  const bool on = k < q.k;
+  uint32_t mine = 0;
+  if (on) mine = word_of(philox4x32_10((uint32_t)k >> 2, q.ctr1, p.step, kStreamGroups, p.key0, p.key1), k & 3);
+  int rank = 0;
+#pragma unroll 1
+  for (int j0 = 0; j0 < q.k; j0 += kPermChunk) {
+    const int nj = min(kPermChunk, q.k - j0);
+    __syncthreads();   // the previous chunk has been read
+    for (int b = threadIdx.x; b < (nj + 3) / 4; b += kPermThreads) {
+      const U32x4 w = philox4x32_10((uint32_t)(j0 / 4 + b), q.ctr1, p.step, kStreamGroups, p.key0, p.key1);
+      keys[b] = make_uint4(w.x, w.y, w.z, w.w);
+    }
+    __syncthreads();
+    if (on) {
+      // keys of indices below k count on ties, the others only when smaller
+      int j = 0;
+#pragma unroll 4
+      for (; j + 4 <= nj; j += 4) {
+        const uint4 v = keys[j / 4];
+        const int jj = j0 + j;
+        rank += (v.x < mine) | ((v.x == mine) & (jj < k));
+        rank += (v.y < mine) | ((v.y == mine) & (jj + 1 < k));
+        rank += (v.z < mine) | ((v.z == mine) & (jj + 2 < k));
+        rank += (v.w < mine) | ((v.w == mine) & (jj + 3 < k));
+      }
+      const uint32_t *tail = reinterpret_cast<const uint32_t *>(keys);
+      for (; j < nj; ++j) rank += (tail[j] < mine) | ((tail[j] == mine) & (j0 + j < k));
+    }
+  }
+  if (on) q.perm[rank] = k;
+}
+
 }  // namespace
 
 hipError_t launch_loss_select(const LossSelectArgs &a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
   hipLaunchKernelGGL(loss_select_kernel, dim3((a.n + 3) / 4), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_group_perm(PermBatch &b, hipStream_t s) {
+  if (b.nl < 1 || b.nl > 8) return hipErrorInvalidValue;
+  int blocks = 0;
+  for (int i = 0; i < b.nl; ++i) {
+    if (b.L[i].k < 1 || b.L[i].perm == nullptr) return hipErrorInvalidValue;
+    b.L[i].block0 = blocks;
+    blocks += (b.L[i].k + kPermThreads - 1) / kPermThreads;
+  }
+  hipLaunchKernelGGL(group_perm_kernel, dim3(blocks), dim3(kPermThreads), 0, s, b);
   return hipGetLastError();
 }
 

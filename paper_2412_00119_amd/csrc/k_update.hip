@@ -331,7 +331,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   for (int mu = tid; mu < p.n; mu += kThreads) {
     const int ks = U.upd[mu] ? kcol[mu] : -1;
     if (ks >= 0) {
-      const int k = g * gamma + ks;
+      const int k = U.perm ? U.perm[g * gamma + ks] : g * gamma + ks;
       const int yl = min(max(p.y[mu], 0), p.c - 1);   // stay inside P on a bad label
       const bool rpos = (U.P[(size_t)yl * U.words_out + (k >> 6)] >> (k & 63)) & 1ull;
       const int pos = atomicAdd(&bucket[ks], 1);
@@ -351,7 +351,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   const int items = gamma * U.chunks;
   for (int it = wave; it < items; it += kWaves) {
     const int r = it / U.chunks, chunk = it - r * U.chunks;
-    const int k = g * gamma + r;
+    const int k = U.perm ? U.perm[g * gamma + r] : g * gamma + r;
     const int cw = chunk * 64 + lane;
     const bool on = cw < U.nw32;
     const int cwc = min(cw, U.nw32 - 1);     // clamped: loads stay inside the rows

@@ -49,7 +49,8 @@ class Pair:
             widths, c, bound, gamma, r, seed,
             fan_in_reinforce=bool(variants & B.BMLP_VARIANT_FAN_IN_REINFORCE),
             shared_classifier=bool(variants & B.BMLP_VARIANT_SHARED_CLASSIFIER),
-            saturate_z=bool(variants & B.BMLP_VARIANT_SATURATE_Z)))
+            saturate_z=bool(variants & B.BMLP_VARIANT_SATURATE_Z),
+            reshuffle_groups=bool(variants & B.BMLP_VARIANT_RESHUFFLE_GROUPS)))
         self.widths = tuple(widths)
         self.c = c
 
@@ -91,7 +92,7 @@ class Pair:
             # restriction to the patterns in M_l (checked through H and stats)
             cfg = self.ora.cfg
             raw = ob.select_easiest(lt.z, self.ora.P[l - 1], np.asarray(y), np.ones(len(y), bool),
-                                    cfg.gamma(self.widths[l]))
+                                    cfg.gamma(self.widths[l]), lt.perm)
             ks = g["kstar"].cpu().numpy()
             np.testing.assert_array_equal(ks, raw, err_msg=f"{tag} kstar_{l}")
             np.testing.assert_array_equal(np.where(lt.upd[:, None], ks, -1), lt.kstar,

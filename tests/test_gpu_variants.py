@@ -1,7 +1,8 @@
 """GPU parity of the method variants (bmlp_config.variants) with the
 oracle, bit for bit, every step: K_{l-1} in the reinforcement probability,
-one classifier shared by every layer, and the selection on z held in
-min(8, ceil(log2(2 K_{l-1}))) bits."""
+one classifier shared by every layer, the selection on z held in
+min(8, ceil(log2(2 K_{l-1}))) bits, and group membership drawn again every
+step."""
 import numpy as np
 import pytest
 
@@ -18,7 +19,9 @@ VARIANTS = {
     "fan_in": B.BMLP_VARIANT_FAN_IN_REINFORCE,
     "shared": B.BMLP_VARIANT_SHARED_CLASSIFIER,
     "saturate": B.BMLP_VARIANT_SATURATE_Z,
-    "all": B.BMLP_VARIANT_FAN_IN_REINFORCE | B.BMLP_VARIANT_SHARED_CLASSIFIER | B.BMLP_VARIANT_SATURATE_Z,
+    "reshuffle": B.BMLP_VARIANT_RESHUFFLE_GROUPS,
+    "all": B.BMLP_VARIANT_FAN_IN_REINFORCE | B.BMLP_VARIANT_SHARED_CLASSIFIER | B.BMLP_VARIANT_SATURATE_Z
+    | B.BMLP_VARIANT_RESHUFFLE_GROUPS,
 }
 
 
@@ -48,3 +51,10 @@ def test_variant_matches_oracle(name, impl):
 def test_saturated_selection_with_gamma_star(impl):
     # gamma* = 105 for 525: the generic selection kernel reads z back
     _run((784, 525), 0, B.BMLP_VARIANT_SATURATE_Z, impl, steps=4)
+
+
+@pytest.mark.parametrize("impl", list(IMPLS))
+def test_reshuffle_large_layer(impl):
+    # K = 2304 spans two key chunks of the order kernel and 9 work-groups;
+    # gamma* = 96 for 2304: 24 groups whose rows come from all over the layer
+    _run((784, 2304), 0, B.BMLP_VARIANT_RESHUFFLE_GROUPS, impl, steps=3)
