@@ -65,6 +65,9 @@ project's design notes):
       group g is positions g*gamma .. g*gamma + gamma - 1 of that order;
       k* is stored as the position within the group, and equal deltas go
       to the lowest perceptron index, as with fixed groups.
+  R21 sequential clipping (the alternative to R8): the selected pairs of
+      the batch are applied in pattern order, each increment clipped to
+      [-B, B] at once; reinforcement and its clip follow as in R8.
 
 Random numbers come from Philox4x32-10 (``oracle.philox``) keyed by the
 64-bit seed (k0 = low word, k1 = high word), with counter
@@ -233,6 +236,7 @@ class Config:
     shared_classifier: bool = False  # one P for every layer (all K_l equal, Section 3.1)
     saturate_z: bool = False         # z held in min(8, ceil(log2(2 K_{l-1}))) bits (Section 3.5)
     reshuffle_groups: bool = False   # random group membership every step (Section 4.3)
+    sequential_clip: bool = False    # the increments applied pattern by pattern, each clipped (R21)
 
     def __post_init__(self):
         self.widths = tuple(int(v) for v in self.widths)
@@ -425,6 +429,19 @@ def clip(h: np.ndarray, bound: int) -> np.ndarray:
     return np.clip(h, -bound, bound)
 
 
+def cp_sequential(H: np.ndarray, S: np.ndarray, a_prev: np.ndarray, bound: int) -> np.ndarray:
+    """The sequential reading of Algorithm 3's increment (R21): pattern by
+    pattern in index order, each selected row gets 2 a^mu rho and is
+    clipped to [-B, B] at once.  Rows selected by one pattern are distinct."""
+    h = H.astype(np.int64).copy()
+    for mu in range(S.shape[0]):
+        ks = np.nonzero(S[mu])[0]
+        if ks.size:
+            inc = 2 * S[mu, ks].astype(np.int64)[:, None] * a_prev[mu].astype(np.int64)[None, :]
+            h[ks] = clip(h[ks] + inc, bound)
+    return h
+
+
 def reinforce(h: np.ndarray, mask: np.ndarray, bound: int) -> np.ndarray:
     """h += 2 sign(h) where the draw fired (Algorithm 3), then clip (R8)."""
     return clip(h + 2 * np.sign(h) * mask.reshape(h.shape), bound)
@@ -477,7 +494,10 @@ def train_step(state: State, x: np.ndarray, y: np.ndarray, t: int, p_r: float,
         if l in want and upd.any():
             # LayerUpdate / PerceptronUpdate run only when M_l is not empty.
             S = selection_matrix(kstar, P, y, gamma, perm)
-            h1 = clip(H.astype(np.int64) + cp_increment(S, a_prev), cfg.bound)
+            if cfg.sequential_clip:
+                h1 = cp_sequential(H, S, a_prev, cfg.bound)
+            else:
+                h1 = clip(H.astype(np.int64) + cp_increment(S, a_prev), cfg.bound)
             kq = kin if cfg.fan_in_reinforce else kout     # R11, or the fan-in variant
             mask = reinforce_mask(cfg.seed, l, t, reinforce_threshold(p_r, kq), kin * kout, kin)
             nreinf = int(mask.sum())

@@ -169,3 +169,64 @@ def test_reshuffle_changes_groups():
         tr = ob.train_step(st.copy(), x, y, 0, 0.0)[0]
         S.append(ob.selection_matrix(tr.kstar, st.P[0], y, 4, tr.perm))
     assert not np.array_equal(S[0], S[1])
+
+
+def test_sequential_clip_order_matters():
+    # h = B, then +2 and -2 from two patterns: one at a time gives B - 2,
+    # the batch sum gives B
+    B = 7
+    H = np.array([[B, -B, 1]], dtype=np.int8)
+    a = np.array([[1, -1, 1], [1, -1, -1]], dtype=np.int8)
+    S = np.array([[1], [-1]], dtype=np.int8)       # rho of the selected row per pattern
+    # column 2 never reaches the bound: 1 + 2 + 2 = 5 either way
+    np.testing.assert_array_equal(ob.cp_sequential(H, S, a, B), [[B - 2, -B + 2, 5]])
+    np.testing.assert_array_equal(ob.clip(H.astype(np.int64) + ob.cp_increment(S, a), B), [[B, -B, 5]])
+
+
+def _brute_sequential(H, S, a, B):
+    h = H.astype(np.int64).tolist()
+    n, k = S.shape
+    for mu in range(n):
+        for kk in range(k):
+            if S[mu, kk]:
+                for i in range(len(h[kk])):
+                    h[kk][i] = max(-B, min(B, h[kk][i] + 2 * int(S[mu, kk]) * int(a[mu, i])))
+    return np.array(h)
+
+
+def test_sequential_clip_brute_force():
+    rng = np.random.default_rng(12)
+    B = 3
+    H = rng.integers(-1, 2, (10, 9)) * 2 + 1
+    H = np.clip(H, -B, B).astype(np.int8)
+    a = random_pm1((30, 9), rng)
+    S = (rng.integers(0, 3, (30, 10)) - 1).astype(np.int8)
+    np.testing.assert_array_equal(ob.cp_sequential(H, S, a, B), _brute_sequential(H, S, a, B))
+
+
+def test_sequential_clip_without_saturation_is_the_sum():
+    # a bound no sum reaches: clipping never acts, both readings agree
+    runs = []
+    for seq in (False, True):
+        cfg = ob.Config((24, 32, 16), 3, 127, 8, 0.5, seed=21, sequential_clip=seq)
+        st = ob.init(cfg)
+        rng = np.random.default_rng(3)
+        for t in range(3):
+            ob.train_step(st, random_pm1((16, 24), rng), rng.integers(0, 3, 16), t, 0.0)
+        runs.append(st)
+    for a_, b_ in zip(runs[0].H, runs[1].H):
+        np.testing.assert_array_equal(a_, b_)
+
+
+def test_sequential_clip_train_step():
+    # B = 1: every increment saturates at once, so the order shows
+    cfg = ob.Config((24, 32), 2, 1, 8, 100.0, seed=5, sequential_clip=True)
+    st = ob.init(cfg)
+    rng = np.random.default_rng(9)
+    x, y = random_pm1((48, 24), rng), rng.integers(0, 2, 48)
+    before = st.copy()
+    tr = ob.train_step(st, x, y, 0, 0.0)[0]
+    S = ob.selection_matrix(tr.kstar, before.P[0], y, 8)
+    np.testing.assert_array_equal(st.H[0], _brute_sequential(before.H[0], S, x, 1))
+    batch = ob.clip(before.H[0].astype(np.int64) + ob.cp_increment(S, x), 1)
+    assert not np.array_equal(st.H[0], batch)
