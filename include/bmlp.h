@@ -81,6 +81,10 @@ enum {
    * is then a position within the group; equal stabilities go to the
    * lowest perceptron index. */
   BMLP_VARIANT_RESHUFFLE_GROUPS = 8,
+  /* the Clipped-Perceptron increments of a step applied pattern by pattern
+   * in index order, each clipped to [-B, B] at once (Algorithm 3 gives no
+   * clip; the default sums the batch's increments and clips once). */
+  BMLP_VARIANT_SEQUENTIAL_CLIP = 16,
 };
 
 /* Limits of this build. */

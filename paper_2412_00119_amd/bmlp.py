@@ -33,6 +33,7 @@ BMLP_VARIANT_FAN_IN_REINFORCE = 1
 BMLP_VARIANT_SHARED_CLASSIFIER = 2
 BMLP_VARIANT_SATURATE_Z = 4
 BMLP_VARIANT_RESHUFFLE_GROUPS = 8
+BMLP_VARIANT_SEQUENTIAL_CLIP = 16
 
 MAX_BATCH = 16384
 

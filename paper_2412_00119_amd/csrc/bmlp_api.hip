@@ -119,7 +119,7 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
     return BMLP_EINVAL;
   constexpr int kAllVariants =
       BMLP_VARIANT_FAN_IN_REINFORCE | BMLP_VARIANT_SHARED_CLASSIFIER | BMLP_VARIANT_SATURATE_Z |
-      BMLP_VARIANT_RESHUFFLE_GROUPS;
+      BMLP_VARIANT_RESHUFFLE_GROUPS | BMLP_VARIANT_SEQUENTIAL_CLIP;
   if (cfg->variants & ~kAllVariants) return BMLP_EINVAL;
   memset(p, 0, sizeof(*p));
   p->variants = cfg->variants;
@@ -561,6 +561,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
   UpdateBatch ub{};
   ub.y = d_y; ub.n = n; ub.ldk = p.max_batch; ub.c = p.c; ub.bound = p.bound;
   ub.key0 = (uint32_t)p.seed; ub.key1 = (uint32_t)(p.seed >> 32); ub.step = (uint32_t)step;
+  ub.sequential = (p.variants & BMLP_VARIANT_SEQUENTIAL_CLIP) ? 1 : 0;
   for (int l = 1; l <= p.L; ++l) {
     const LayerPlan &lp = p.layer[l - 1];
     UpdLayer &u = ub.L[ub.nl++];

@@ -179,6 +179,7 @@ struct UpdateBatch {
   const int32_t *y;
   int n, ldk, c, bound;
   uint32_t key0, key1, step;
+  int sequential;          // increments applied pattern by pattern, each clipped
 };
 hipError_t launch_update(UpdateBatch &b, hipStream_t s);
 

@@ -255,6 +255,32 @@ __device__ __forceinline__ uint32_t equals(const uint32_t (&u)[M], int v) {
   return e;
 }
 
+// The sequential reading of the increments: the row's S >= 1 selectors
+// (list[beg .. beg+S), in pattern order) one at a time, each moving u by +1
+// where a rho = +1 and -1 elsewhere, clipped to [0, B] at once.  Columns
+// outside validmask keep their value.
+template <int M>
+__device__ __forceinline__ void cp_sequential(uint32_t (&u)[M], const uint16_t *list, int beg, int S, int B,
+                                              uint32_t validmask, const uint32_t *a32, int nw32, int cw) {
+  for (int s = 0; s < S; ++s) {
+    const uint32_t ent = __builtin_amdgcn_readfirstlane(list[beg + s]);
+    const uint32_t mu = ent & 0x7FFFu;
+    const uint32_t x = a32[(size_t)mu * nw32 + cw] ^ ((ent & 0x8000u) ? 0xFFFFFFFFu : 0u);
+    const uint32_t inc = x & validmask & ~equals<M>(u, B);
+    const uint32_t dec = ~x & validmask & ~equals<M>(u, 0);
+    const uint32_t g = inc | dec;
+    // u + 1 on inc, u + (2^M - 1) = u - 1 on dec
+    uint32_t carry = u[0] & g;
+    u[0] ^= g;
+#pragma unroll
+    for (int q = 1; q < M; ++q) {
+      const uint32_t sum = u[q] ^ dec ^ carry;
+      carry = maj(u[q], dec, carry);
+      u[q] = sum;
+    }
+  }
+}
+
 // Lanes where the M-plane value is at least the constant k (0 < k <= 2^M):
 // the sign plane of u - k in M + 1 bits is clear.
 template <int M>
@@ -328,14 +354,41 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     }
   }
   __syncthreads();
-  for (int mu = tid; mu < p.n; mu += kThreads) {
-    const int ks = U.upd[mu] ? kcol[mu] : -1;
-    if (ks >= 0) {
-      const int k = U.perm ? U.perm[g * gamma + ks] : g * gamma + ks;
-      const int yl = min(max(p.y[mu], 0), p.c - 1);   // stay inside P on a bad label
-      const bool rpos = (U.P[(size_t)yl * U.words_out + (k >> 6)] >> (k & 63)) & 1ull;
-      const int pos = atomicAdd(&bucket[ks], 1);
-      list[pos] = (uint16_t)(mu | (rpos ? 0 : 0x8000));
+  if (!p.sequential) {
+    for (int mu = tid; mu < p.n; mu += kThreads) {
+      const int ks = U.upd[mu] ? kcol[mu] : -1;
+      if (ks >= 0) {
+        const int k = U.perm ? U.perm[g * gamma + ks] : g * gamma + ks;
+        const int yl = min(max(p.y[mu], 0), p.c - 1);   // stay inside P on a bad label
+        const bool rpos = (U.P[(size_t)yl * U.words_out + (k >> 6)] >> (k & 63)) & 1ull;
+        const int pos = atomicAdd(&bucket[ks], 1);
+        list[pos] = (uint16_t)(mu | (rpos ? 0 : 0x8000));
+      }
+    }
+  } else if (wave == 0) {
+    // the same lists, each in pattern order: wave 0 walks the patterns 64
+    // at a time, and the lanes that share a row take consecutive slots in
+    // lane order
+    for (int base = 0; base < p.n; base += 64) {
+      const int mu = base + lane;
+      const int ks = (mu < p.n && U.upd[mu]) ? kcol[mu] : -1;
+      uint32_t ent = 0u;
+      if (ks >= 0) {
+        const int k = U.perm ? U.perm[g * gamma + ks] : g * gamma + ks;
+        const int yl = min(max(p.y[mu], 0), p.c - 1);
+        const bool rpos = (U.P[(size_t)yl * U.words_out + (k >> 6)] >> (k & 63)) & 1ull;
+        ent = (uint32_t)mu | (rpos ? 0u : 0x8000u);
+      }
+      uint64_t pending = __ballot(ks >= 0);
+      while (pending) {
+        const int leader = __ffsll((unsigned long long)pending) - 1;
+        const int key = __shfl(ks, leader, 64);
+        const uint64_t same = __ballot(ks == key) & pending;
+        const int start = bucket[key];
+        if (lane == leader) bucket[key] = start + __popcll(same);
+        if ((same >> lane) & 1ull) list[start + __popcll(same & ((1ull << lane) - 1ull))] = (uint16_t)ent;
+        pending &= ~same;
+      }
     }
   }
   __syncthreads();
@@ -381,7 +434,9 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     const U32x4 v1 = philox4x32_10(blk + 1u, U.ctr1, p.step, kStreamCoarse, key0, key1);
 
     // ---- Clipped-Perceptron sum and clip ------------------------------------
-    if (S > 0) {
+    if (S > 0 && p.sequential) {
+      cp_sequential<M>(u, list, beg, S, Bi, validmask, U.a32, U.nw32, cwc);
+    } else if (S > 0) {
       uint32_t c[kPlanes];
       count_row(c, list, beg, S, U.a32, U.nw32, cwc);
       uint32_t un[M];

@@ -50,7 +50,8 @@ class Pair:
             fan_in_reinforce=bool(variants & B.BMLP_VARIANT_FAN_IN_REINFORCE),
             shared_classifier=bool(variants & B.BMLP_VARIANT_SHARED_CLASSIFIER),
             saturate_z=bool(variants & B.BMLP_VARIANT_SATURATE_Z),
-            reshuffle_groups=bool(variants & B.BMLP_VARIANT_RESHUFFLE_GROUPS)))
+            reshuffle_groups=bool(variants & B.BMLP_VARIANT_RESHUFFLE_GROUPS),
+            sequential_clip=bool(variants & B.BMLP_VARIANT_SEQUENTIAL_CLIP)))
         self.widths = tuple(widths)
         self.c = c
 

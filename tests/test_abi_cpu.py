@@ -149,7 +149,7 @@ def test_variants_validated_and_shared_classifier_held_once():
     # unequal widths cannot share a classifier; unknown variant bits are refused
     assert B.bmlp_state_bytes(B.make_config((20, 16, 8), 3, 7, 8, group_size=4,
                                             variants=B.BMLP_VARIANT_SHARED_CLASSIFIER)) == 0
-    assert B.bmlp_state_bytes(B.make_config((20, 16), 3, 7, 8, group_size=4, variants=16)) == 0
+    assert B.bmlp_state_bytes(B.make_config((20, 16), 3, 7, 8, group_size=4, variants=32)) == 0
 
 
 def test_input_side_shapes_rejected_before_any_launch():

@@ -1,8 +1,10 @@
 """GPU parity of the method variants (bmlp_config.variants) with the
 oracle, bit for bit, every step: K_{l-1} in the reinforcement probability,
 one classifier shared by every layer, the selection on z held in
-min(8, ceil(log2(2 K_{l-1}))) bits, and group membership drawn again every
-step."""
+min(8, ceil(log2(2 K_{l-1}))) bits, group membership drawn again every
+step, and the increments clipped pattern by pattern."""
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -20,8 +22,9 @@ VARIANTS = {
     "shared": B.BMLP_VARIANT_SHARED_CLASSIFIER,
     "saturate": B.BMLP_VARIANT_SATURATE_Z,
     "reshuffle": B.BMLP_VARIANT_RESHUFFLE_GROUPS,
+    "sequential": B.BMLP_VARIANT_SEQUENTIAL_CLIP,
     "all": B.BMLP_VARIANT_FAN_IN_REINFORCE | B.BMLP_VARIANT_SHARED_CLASSIFIER | B.BMLP_VARIANT_SATURATE_Z
-    | B.BMLP_VARIANT_RESHUFFLE_GROUPS,
+    | B.BMLP_VARIANT_RESHUFFLE_GROUPS | B.BMLP_VARIANT_SEQUENTIAL_CLIP,
 }
 
 
@@ -58,3 +61,23 @@ def test_reshuffle_large_layer(impl):
     # K = 2304 spans two key chunks of the order kernel and 9 work-groups;
     # gamma* = 96 for 2304: 24 groups whose rows come from all over the layer
     _run((784, 2304), 0, B.BMLP_VARIANT_RESHUFFLE_GROUPS, impl, steps=3)
+
+
+@pytest.mark.parametrize("impl", list(IMPLS))
+def test_sequential_clip_saturating(impl):
+    # B = 3 with prototype data: rows saturate within a step, so the order of
+    # the increments shows; gamma = 16 gives 64 selections per pattern
+    w = synth.TINY
+    p = Pair((784, 1024), w.n_classes, 3, w.batch, 16, 0.25, seed=23, fwd_impl=IMPLS[impl],
+             variants=B.BMLP_VARIANT_SEQUENTIAL_CLIP)
+    d = synth.make_split(w, "train", n=3 * w.batch)
+    order_showed = False
+    for t, (x, y) in enumerate(d.batches(w.batch)):
+        note(f"sequential clip impl {impl} step {t}")
+        # the batch reading from the same state, on the CPU
+        alt = p.ora.copy()
+        alt.cfg = dataclasses.replace(p.ora.cfg, sequential_clip=False)
+        ob.train_step(alt, x, y, t, 0.5)
+        p.step(x, y, t, 0.5, tag=f"step {t}")
+        order_showed |= not np.array_equal(alt.H[0], p.ora.H[0])
+    assert order_showed
