@@ -81,3 +81,30 @@ def test_sequential_clip_saturating(impl):
         p.step(x, y, t, 0.5, tag=f"step {t}")
         order_showed |= not np.array_equal(alt.H[0], p.ora.H[0])
     assert order_showed
+
+
+RAGGED = [
+    # widths, c, B, gamma, n, steps, p_r, r
+    ((37, 24, 12), 3, 5, 4, 9, 4, 2.0, 0.25),          # K_l not a multiple of 4 or 64
+    ((70, 60, 60), 5, 1, 6, 33, 3, 0.5, 0.25),          # B = 1
+    ((1000, 525), 10, 15, 0, 100, 3, 0.5, 0.25),        # gamma* = 105
+    ((200, 135, 135), 10, 3, 0, 64, 3, 0.5, 0.25),      # gamma* = 135, B = 3
+]
+
+
+@pytest.mark.parametrize("impl", list(IMPLS))
+@pytest.mark.parametrize("case", RAGGED, ids=[f"{c[0]}-B{c[2]}-g{c[3]}-n{c[4]}" for c in RAGGED])
+def test_all_variants_ragged(case, impl):
+    widths, c, bound, gamma, n, steps, p_r, r = case
+    v = (B.BMLP_VARIANT_FAN_IN_REINFORCE | B.BMLP_VARIANT_SATURATE_Z | B.BMLP_VARIANT_RESHUFFLE_GROUPS
+         | B.BMLP_VARIANT_SEQUENTIAL_CLIP)
+    if len(set(widths[1:])) == 1:
+        v |= B.BMLP_VARIANT_SHARED_CLASSIFIER
+    rng = np.random.default_rng(sum(widths) + n + 7)
+    p = Pair(widths, c, bound, n + 3, gamma, r, seed=int(rng.integers(1 << 62)), fwd_impl=IMPLS[impl],
+             variants=v)
+    for t in range(steps):
+        note(f"variants {v} shape {widths} step {t}")
+        x = synth.random_pm1((n, widths[0]), rng)
+        y = rng.integers(0, c, size=n).astype(np.int32)
+        p.step(x, y, 500 + t, p_r, tag=f"step {t}")
