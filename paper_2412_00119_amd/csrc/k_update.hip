@@ -299,7 +299,8 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   __shared__ int s_sel;
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+  // the wave index is uniform: in a scalar register, so are the item indices
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   // ---- which layer / group ---------------------------------------------------
   int li = 0;
 #pragma unroll 1
