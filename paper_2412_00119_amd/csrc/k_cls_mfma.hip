@@ -86,7 +86,7 @@ __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
   int (*red)[16][CB * 16] = reinterpret_cast<int (*)[16][CB * 16]>(lds);   // per K group; red[0] ends with y_hat
   __shared__ int cnt[3];                 // block totals of err, upd, correct
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int kg = wave % KG, cg = wave / KG;
   const int bpl = (p.n + 15) / 16;               // work-groups per layer
   const ClsLayer &Lr = p.L[blockIdx.x / bpl];

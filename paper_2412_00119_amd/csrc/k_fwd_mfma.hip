@@ -131,7 +131,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   constexpr int kIssue = 2 * kDma;                // loads per wave and step
   static_assert(kIssue * (kStages - 2) < 64, "vmcnt range");
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
   int mt, nt;
   {
