@@ -27,7 +27,7 @@
 //   * h <- h + 2 sign(h) is u <- u +- 1 on the fired columns, one more planar
 //     addition, and W = sign(H) is u >= (B + 1) / 2.
 //
-// Work-group: (layer, group g), 16 waves.  The group's selections U_l (each
+// Work-group: (layer, group g, half of g's rows), 12 waves.  The group's selections U_l (each
 // pattern in M_l with a wrong perceptron in the group) are bucketed by
 // perceptron in LDS (counting sort), then the waves take the group's (row,
 // 2048-column chunk) items, lane l owning 32-column group chunk * 64 + l.  No
@@ -38,8 +38,13 @@
 namespace bmlp {
 namespace {
 
-constexpr int kWaves = 16;
+// Two work-groups of 12 waves per group of perceptrons, each taking half
+// of the group's rows: two of them fit a compute unit together (six waves
+// per SIMD), which hides more of the H loads behind the draws than one
+// work-group of 16 waves per compute unit did.
+constexpr int kWaves = 12;
 constexpr int kThreads = 64 * kWaves;
+constexpr int kSplit = 2;
 constexpr int kPlanes = 15;   // counts up to 2^15 - 1 >= BMLP_MAX_BATCH
 
 // A wave-uniform word the compiler must treat as unknown and keep in a
@@ -308,7 +313,8 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     if ((int)blockIdx.x >= p.L[i].block0) li = i;
   const UpdLayer &U = p.L[li];
   if (U.stats[1] == 0) return;   // M_l empty: Algorithm 2 is not run for this layer
-  const int g = (int)blockIdx.x - U.block0;
+  const int g = ((int)blockIdx.x - U.block0) / kSplit;
+  const int part = ((int)blockIdx.x - U.block0) % kSplit;
   const int gamma = U.gamma;
   int *bucket = smem;                                            // [gamma]
   uint16_t *list = reinterpret_cast<uint16_t *>(smem + gamma);   // [n]
@@ -402,9 +408,11 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
 
   // work items: (row r, 2048-column chunk); lane l owns 32-column group
   // chunk * 64 + l of the row
-  const int items = gamma * U.chunks;
+  // this work-group's rows: [r_lo, r_hi) of the group
+  const int r_lo = part * gamma / kSplit, r_hi = (part + 1) * gamma / kSplit;
+  const int items = (r_hi - r_lo) * U.chunks;
   for (int it = wave; it < items; it += kWaves) {
-    const int r = it / U.chunks, chunk = it - r * U.chunks;
+    const int r = r_lo + it / U.chunks, chunk = it % U.chunks;
     const int k = U.perm ? U.perm[g * gamma + r] : g * gamma + r;
     const int cw = chunk * 64 + lane;
     const bool on = cw < U.nw32;
@@ -523,7 +531,9 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     for (int w = 0; w < kWaves; ++w) t += wsum[w];
     // |U_l| and the reinforced draws are adjacent 32-bit counts of the
     // layer's stats row: one 64-bit atomic per work-group adds both
-    const unsigned long long v = (unsigned long long)(uint32_t)s_sel | ((unsigned long long)(uint32_t)t << 32);
+    // |U_l| of the group once, from its first work-group
+    const uint32_t sel = part == 0 ? (uint32_t)s_sel : 0u;
+    const unsigned long long v = (unsigned long long)sel | ((unsigned long long)(uint32_t)t << 32);
     if (v) atomicAdd(reinterpret_cast<unsigned long long *>(U.stats + 2), v);
   }
 }
@@ -542,7 +552,7 @@ hipError_t launch_update(UpdateBatch &b, hipStream_t s) {
     UpdLayer &u = b.L[i];
     u.chunks = (u.nw32 + 63) / 64;
     u.block0 = blocks;
-    blocks += u.groups;
+    blocks += u.groups * kSplit;
     gmax = max(gmax, u.gamma);
   }
   const dim3 grid(blocks), block(kThreads);
