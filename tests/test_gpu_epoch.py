@@ -47,6 +47,18 @@ def test_tiny_workload_two_epochs(impl):
     _epochs(p, d.x, d.y, w.batch, 2, w.p_r, seed=3)
 
 
+def test_epochs_with_every_variant():
+    # the epoch driver runs the variant step: reshuffled groups, sequential
+    # clipping, saturated z, fan-in reinforcement and one shared classifier
+    from paper_2412_00119_amd import bmlp as B
+    v = (B.BMLP_VARIANT_FAN_IN_REINFORCE | B.BMLP_VARIANT_SHARED_CLASSIFIER | B.BMLP_VARIANT_SATURATE_Z
+         | B.BMLP_VARIANT_RESHUFFLE_GROUPS | B.BMLP_VARIANT_SEQUENTIAL_CLIP)
+    w = synth.TINY
+    p = Pair((784, 256, 256), w.n_classes, 7, w.batch, 32, w.robustness, w.seed_model, variants=v)
+    d = synth.make_split(w, "train", n=600)
+    _epochs(p, d.x, d.y, w.batch, 2, w.p_r, seed=9)
+
+
 def test_ragged_shapes_epochs():
     # odd word counts (37, 130 inputs), gamma* = 105, batch below max_batch
     p = Pair((130, 525, 37), 7, 9, 64, 0, 0.25, seed=21)
