@@ -69,6 +69,11 @@ project's design notes):
       the batch are applied in pattern order, each increment clipped to
       [-B, B] at once; reinforcement and its clip follow as in R8.
 
+Parity unpinned: the paper does not fix readings R1, R2, R5 (its tie
+rule), R11, R17, R18, R19, R20, R21 or the Philox stream layout below, so
+nothing outside this code decides them; the arithmetic of each is still
+pinned by the tests (brute force, hand-computed cases, direct Philox calls).
+
 Random numbers come from Philox4x32-10 (``oracle.philox``) keyed by the
 64-bit seed (k0 = low word, k1 = high word), with counter
 (block, l-1, t mod 2^32, stream):
