@@ -31,6 +31,7 @@
 // Work-groups are mapped so that each XCD (work-group id mod 8) works on
 // its own slice of W_l, which then stays in that XCD's L2.
 #include <algorithm>
+#include <type_traits>
 
 #include "bmlp_internal.h"
 #include "fp4.h"
@@ -388,22 +389,31 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
       // every right one (t < 0, sign bit set) comes after them.
       const uint32_t sh = 31u - (uint32_t)lc;
       uint32_t v[32];
+      // z as the selection sees it: clipped only where [zlo, zhi] is
+      // narrower than every |z| <= 32767 (the saturating variant)
+      auto keys = [&](auto clip_tag) {
+        constexpr bool kClip = decltype(clip_tag)::value;
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int rl = wm * 64 + i * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
-          const uint64_t rho = sP[wn][rl];
-          uint32_t key[2];
+          for (int e = 0; e < 16; ++e) {
+            const int rl = wm * 64 + i * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
+            const uint64_t rho = sP[wn][rl];
+            uint32_t key[2];
 #pragma unroll
-          for (int j = 0; j < 2; ++j) {
-            const uint32_t r = (uint32_t)(rho >> (32 * j)) << sh;   // bit 31: rho of column j*32 + lc
-            const float zc = fminf(fmaxf(acc[i][j][e], p.zlo), p.zhi);   // z as the selection sees it
-            const float sz = __uint_as_float(__float_as_uint(zc) ^ (r & 0x80000000u));
-            key[j] = __float_as_uint(sz - 0.5f) | (uint32_t)(j * 32 + lc);
+            for (int j = 0; j < 2; ++j) {
+              const uint32_t r = (uint32_t)(rho >> (32 * j)) << sh;   // bit 31: rho of column j*32 + lc
+              const float zc = kClip ? fminf(fmaxf(acc[i][j][e], p.zlo), p.zhi) : acc[i][j][e];
+              const float sz = __uint_as_float(__float_as_uint(zc) ^ (r & 0x80000000u));
+              key[j] = __float_as_uint(sz - 0.5f) | (uint32_t)(j * 32 + lc);
+            }
+            v[i * 16 + e] = min(key[0], key[1]);
           }
-          v[i * 16 + e] = min(key[0], key[1]);
-        }
+      };
+      if (p.zlo > -32767.f || p.zhi < 32767.f)
+        keys(std::true_type{});
+      else
+        keys(std::false_type{});
       // Reduce-scatter over the 32 lanes of a half-wave: at each step a lane
       // keeps half of its rows (the upper half if the step's lane bit is
       // set) and takes the minimum with a partner's copy of those rows.
