@@ -161,3 +161,32 @@ def test_resume_from_state_is_exact():
         c.train_step(xb, yt, t, 0.5)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(a.state.cpu().numpy(), c.state.cpu().numpy())
+
+
+@pytest.mark.parametrize("impl", list(IMPLS))
+@pytest.mark.parametrize("variants", [0, 16], ids=["batch_clip", "sequential_clip"])
+def test_maximum_batch(impl, variants):
+    # 16384 patterns, the most the library takes (the update's selector
+    # entries keep a pattern index in 15 bits, the sign of rho in the 16th)
+    n = 16384
+    rng = np.random.default_rng(77)
+    p = Pair((64, 128, 64), 10, 7, n, 16, 0.25, seed=99, fwd_impl=IMPLS[impl], variants=variants)
+    for t in range(2):
+        note(f"maximum batch {n} variants {variants} step {t}")
+        x = random_pm1((n, 64), rng)
+        y = rng.integers(0, 10, size=n).astype(np.int32)
+        p.step(x, y, t, 0.5, tag=f"step {t}")
+
+
+@pytest.mark.parametrize("impl", list(IMPLS))
+def test_maximum_width(impl):
+    # K_1 = 32767, the widest layer the library takes (|z| of layer 2 is
+    # bounded by 32767, int16's range): gamma* = 31, 1057 groups, and
+    # layer 2 reads 1024-word rows
+    rng = np.random.default_rng(78)
+    p = Pair((64, 32767, 48), 5, 7, 256, 0, 0.25, seed=98, fwd_impl=IMPLS[impl])
+    for t in range(2):
+        note(f"maximum width step {t}")
+        x = random_pm1((256, 64), rng)
+        y = rng.integers(0, 5, size=256).astype(np.int32)
+        p.step(x, y, t, 0.5, tag=f"step {t}")
