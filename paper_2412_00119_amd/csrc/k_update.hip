@@ -297,7 +297,26 @@ __device__ __forceinline__ uint32_t at_least(const uint32_t (&u)[M], int k) {
   return ~sign_of_sum<M + 1>(x, (uint32_t)(-k));
 }
 
+// Lanes whose M-plane value has every plane set / any plane set.
 template <int M>
+__device__ __forceinline__ uint32_t all_planes(const uint32_t (&u)[M]) {
+  uint32_t e = u[0];
+#pragma unroll
+  for (int q = 1; q < M; ++q) e &= u[q];
+  return e;
+}
+template <int M>
+__device__ __forceinline__ uint32_t any_plane(const uint32_t (&u)[M]) {
+  uint32_t e = u[0];
+#pragma unroll
+  for (int q = 1; q < M; ++q) e |= u[q];
+  return e;
+}
+
+// FULL: B = 2^M - 1 (B = 1, 3, 7, 15, 31, 63, 127), so u = B is every plane
+// set and u >= (B + 1) / 2 is the top plane; otherwise the planar
+// comparisons with the constants of B.
+template <int M, bool FULL>
 __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   extern __shared__ int smem[];
   __shared__ int wsum[kWaves];
@@ -462,7 +481,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
       for (int q = 0; q < M; ++q) u[q] = (un[q] & validmask) | (u[q] & ~validmask);
     }
     // sign(h) after the Clipped-Perceptron step; reinforcement keeps it
-    const uint32_t pos = at_least<M>(u, (Bi + 1) >> 1);
+    const uint32_t pos = FULL ? u[M - 1] : at_least<M>(u, (Bi + 1) >> 1);
 
     // ---- which weights reinforce: u8 < T >> 24, or u8 == T >> 24 and the
     // fine 24 bits below T & 0xFFFFFF ---------------------------------------------
@@ -501,7 +520,8 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     // ---- h <- clip(h + 2 sign(h)) on the fired weights, i.e. u <- u + 1 where
     // h > 0 and u - 1 where h < 0; |h| = B (u = 0 or B) stays -------------------
     {
-      const uint32_t gmask = fire & ~(equals<M>(u, 0) | equals<M>(u, Bi));
+      const uint32_t at_bound = FULL ? (~any_plane<M>(u) | all_planes<M>(u)) : (equals<M>(u, 0) | equals<M>(u, Bi));
+      const uint32_t gmask = fire & ~at_bound;
       const uint32_t dn = gmask & ~pos;   // delta -1 = all ones
       uint32_t carry = u[0] & gmask;
       u[0] ^= gmask;
@@ -538,6 +558,14 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   }
 }
 
+template <int M>
+void launch_planes(bool full, dim3 grid, dim3 block, size_t lds, hipStream_t s, const UpdateBatch &b) {
+  if (full)
+    hipLaunchKernelGGL((update_kernel<M, true>), grid, block, lds, s, b);
+  else
+    hipLaunchKernelGGL((update_kernel<M, false>), grid, block, lds, s, b);
+}
+
 }  // namespace
 
 size_t update_lds_bytes(int gamma, int n) {
@@ -557,14 +585,15 @@ hipError_t launch_update(UpdateBatch &b, hipStream_t s) {
   }
   const dim3 grid(blocks), block(kThreads);
   const size_t lds = update_lds_bytes(gmax, b.n);
+  const bool full = b.bound == (1 << h_planes(b.bound)) - 1;
   switch (h_planes(b.bound)) {
-    case 1: hipLaunchKernelGGL(update_kernel<1>, grid, block, lds, s, b); break;
-    case 2: hipLaunchKernelGGL(update_kernel<2>, grid, block, lds, s, b); break;
-    case 3: hipLaunchKernelGGL(update_kernel<3>, grid, block, lds, s, b); break;
-    case 4: hipLaunchKernelGGL(update_kernel<4>, grid, block, lds, s, b); break;
-    case 5: hipLaunchKernelGGL(update_kernel<5>, grid, block, lds, s, b); break;
-    case 6: hipLaunchKernelGGL(update_kernel<6>, grid, block, lds, s, b); break;
-    default: hipLaunchKernelGGL(update_kernel<7>, grid, block, lds, s, b); break;
+    case 1: launch_planes<1>(full, grid, block, lds, s, b); break;
+    case 2: launch_planes<2>(full, grid, block, lds, s, b); break;
+    case 3: launch_planes<3>(full, grid, block, lds, s, b); break;
+    case 4: launch_planes<4>(full, grid, block, lds, s, b); break;
+    case 5: launch_planes<5>(full, grid, block, lds, s, b); break;
+    case 6: launch_planes<6>(full, grid, block, lds, s, b); break;
+    default: launch_planes<7>(full, grid, block, lds, s, b); break;
   }
   return hipGetLastError();
 }
