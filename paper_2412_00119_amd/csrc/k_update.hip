@@ -492,11 +492,17 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     } else {
       const uint32_t rp[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
       uint32_t lt = 0u, eq = 0xFFFFFFFFu;
+      // from the top bit: u8 < t_hi or still equal.  Bit q of t_hi is
+      // uniform, so each plane takes a scalar branch and one or two
+      // bitwise operations instead of three.
 #pragma unroll
-      for (int q = 7; q >= 0; --q) {   // from the top bit: u8 < t_hi or still equal
-        const uint32_t tb = plane_of(thi, q);
-        lt |= eq & ~rp[q] & tb;
-        eq &= ~(rp[q] ^ tb);
+      for (int q = 7; q >= 0; --q) {
+        if ((thi >> q) & 1u) {
+          lt |= eq & ~rp[q];
+          eq &= rp[q];
+        } else {
+          eq &= ~rp[q];
+        }
       }
       fire = lt;
       need = eq;
