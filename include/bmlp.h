@@ -293,6 +293,18 @@ int bmlp_train_epoch(bmlp_ctx *ctx, const uint64_t *d_x_all, const int32_t *d_y_
  * sample was trained on.  Host only. */
 double bmlp_epoch_rescale(double p_r, int64_t wrong, int64_t samples);
 
+/* The end of an epoch from its step counts (Algorithm 1's epoch loop; Section
+ * 3.4, reading R16): h_stats is a host copy of the d_stats that
+ * bmlp_train_epoch filled, int32 [steps][n_layers][BMLP_STATS_STRIDE];
+ * wrong = the sum over the steps of entry 0 (01-loss count) of the last
+ * layer's row, samples = steps * batch.  Writes E^e = wrong / samples to
+ * *h_error_fraction (NaN when steps = 0) and bmlp_epoch_rescale(p_r, wrong,
+ * samples) to *h_p_r_next; either pointer may be NULL.  Host only; returns
+ * BMLP_EINVAL for a NULL h_stats with steps > 0, BMLP_ESHAPE for negative
+ * sizes or a layer count outside 1..BMLP_MAX_LAYERS. */
+int bmlp_epoch_summary(const int32_t *h_stats, int32_t steps, int32_t n_layers, int32_t batch, double p_r,
+                       double *h_error_fraction, double *h_p_r_next);
+
 /* Device pointers to H_l (bit-sliced, see bmlp_layer_info), W_l and P_l of
  * layer l (1..L) in the state. */
 int bmlp_layer_views(bmlp_ctx *ctx, int32_t l, uint8_t **d_h, uint64_t **d_w, uint64_t **d_p);

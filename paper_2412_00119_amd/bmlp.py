@@ -100,6 +100,8 @@ def lib() -> ctypes.CDLL:
             "bmlp_expand": (ctypes.c_int, [vp, i32, i32, i32, u64, vp, vp]),
             "bmlp_train_epoch": (ctypes.c_int, [vp, vp, vp, i32, vp, i32, i32, u64, dbl, vp, vp]),
             "bmlp_epoch_rescale": (dbl, [dbl, ctypes.c_int64, ctypes.c_int64]),
+            "bmlp_epoch_summary": (ctypes.c_int, [vp, i32, i32, i32, dbl, ctypes.POINTER(dbl),
+                                                  ctypes.POINTER(dbl)]),
             "bmlp_layer_views": (ctypes.c_int, [vp, i32, ctypes.POINTER(vp), ctypes.POINTER(vp),
                                                 ctypes.POINTER(vp)]),
             "bmlp_step_trace": (ctypes.c_int, [vp, i32, ctypes.POINTER(vp), ctypes.POINTER(vp),
@@ -251,6 +253,14 @@ def bmlp_epoch_rescale(p_r: float, wrong: int, samples: int) -> float:
     return lib().bmlp_epoch_rescale(p_r, wrong, samples)
 
 
+def bmlp_epoch_summary(h_stats: int, steps: int, n_layers: int, batch: int, p_r: float):
+    """(E^e, p_r for the next epoch) from a host copy of an epoch's stats."""
+    e, nxt = ctypes.c_double(), ctypes.c_double()
+    _check(lib().bmlp_epoch_summary(h_stats, steps, n_layers, batch, p_r, ctypes.byref(e), ctypes.byref(nxt)),
+           "bmlp_epoch_summary")
+    return e.value, nxt.value
+
+
 def bmlp_read_h(ctx: int, layer: int, d_out: int, stream: int):
     _check(lib().bmlp_read_h(ctx, layer, d_out, stream), "bmlp_read_h")
 
@@ -386,10 +396,9 @@ class BMLP:
         bmlp_train_epoch(self.ctx, x_bits_all.data_ptr(), y_all.data_ptr(), x_bits_all.shape[0],
                          order.data_ptr(), order.shape[0], batch, int(step0), float(p_r), stats.data_ptr(),
                          self._stream())
-        counts = stats[:nb, :, :4].cpu()   # waits for the stream
-        wrong = int(counts[:, -1, 0].sum()) if nb else 0
-        e = wrong / (nb * batch) if nb else float("nan")
-        return bmlp_epoch_rescale(float(p_r), wrong, nb * batch), e, counts
+        host = stats.cpu()   # waits for the stream
+        e, p_next = bmlp_epoch_summary(host.data_ptr(), nb, self.n_layers, batch, float(p_r))
+        return p_next, e, host[:nb, :, :4]
 
     def eval_exit(self, x_bits, y, counts=None):
         """Adds per layer [correct, exits, correct exits] of this batch to

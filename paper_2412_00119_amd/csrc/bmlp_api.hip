@@ -446,6 +446,19 @@ double bmlp_epoch_rescale(double p_r, int64_t wrong, int64_t samples) {
   return p_r * sqrt((double)wrong / (double)samples);
 }
 
+int bmlp_epoch_summary(const int32_t *h_stats, int32_t steps, int32_t n_layers, int32_t batch, double p_r,
+                       double *h_error_fraction, double *h_p_r_next) {
+  if (steps < 0 || batch < 0 || n_layers < 1 || n_layers > BMLP_MAX_LAYERS) return BMLP_ESHAPE;
+  if (steps > 0 && h_stats == nullptr) return BMLP_EINVAL;
+  int64_t wrong = 0;
+  for (int32_t b = 0; b < steps; ++b)
+    wrong += h_stats[((size_t)b * n_layers + (n_layers - 1)) * BMLP_STATS_STRIDE];
+  const int64_t samples = (int64_t)steps * batch;
+  if (h_error_fraction) *h_error_fraction = samples > 0 ? (double)wrong / (double)samples : NAN;
+  if (h_p_r_next) *h_p_r_next = bmlp_epoch_rescale(p_r, wrong, samples);
+  return BMLP_OK;
+}
+
 int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int32_t n,
                     uint64_t step, double p_r, int32_t *d_stats, void *stream) {
   int st = check_ctx_batch(ctx, d_x, n);

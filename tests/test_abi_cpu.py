@@ -158,3 +158,24 @@ def test_input_side_shapes_rejected_before_any_launch():
     assert B.lib().bmlp_expand(None, 4, 10, 64, 1, None, None) == B.BMLP_EINVAL
     assert B.lib().bmlp_feature_median(None, 0, 8, None, None) == B.BMLP_ESHAPE
     assert B.lib().bmlp_binarize(None, 3, 8, None, None, None) == B.BMLP_EINVAL
+
+
+def test_epoch_summary_from_counts():
+    # E^e = last-layer errors / samples and p_r sqrt(E^e) (Alg. 1's epoch
+    # loop, Sec. 3.4), from a host copy of the epoch's stats rows
+    import ctypes
+    import math
+    import numpy as np
+    from paper_2412_00119_amd import bmlp as B
+    steps, L, batch = 3, 2, 10
+    st = np.zeros((steps, L, B.STATS_STRIDE), dtype=np.int32)
+    st[:, 1, 0] = [2, 0, 5]     # last layer's 01-loss counts
+    st[:, 0, 0] = [9, 9, 9]     # other layers do not count
+    e, nxt = B.bmlp_epoch_summary(st.ctypes.data, steps, L, batch, 0.5)
+    assert e == 7 / 30 and nxt == 0.5 * math.sqrt(7 / 30)
+    e, nxt = B.bmlp_epoch_summary(0, 0, L, batch, 0.5)
+    assert math.isnan(e) and nxt == 0.5
+    with pytest.raises(B.BmlpError):
+        B.bmlp_epoch_summary(0, 2, L, batch, 0.5)
+    with pytest.raises(B.BmlpError):
+        B.bmlp_epoch_summary(st.ctypes.data, steps, 0, batch, 0.5)

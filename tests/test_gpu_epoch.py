@@ -8,7 +8,7 @@ import pytest
 import oracle.bmlp as ob
 from paper_2412_00119_amd import synth
 
-from gpu_common import Pair, note, torch_cuda
+from gpu_common import Pair, note, pack_np, torch_cuda
 
 pytestmark = pytest.mark.gpu
 
@@ -91,3 +91,54 @@ def test_early_exit_matches(impl, r):
     got = p.gpu.eval_exit(xb[200:], yt[200:], got)    # counts add up over batches
     p.torch.cuda.synchronize()
     np.testing.assert_array_equal(got.cpu().numpy(), ob.early_exit(p.ora, te.x, te.y))
+
+
+def test_small_workload_five_epochs():
+    # The 784 -> 1024 -> 1024 workload over its whole schedule: five epochs of
+    # 234 full batches of 256 through bmlp_train_epoch, the p_r rescale after
+    # each (Alg. 1's epoch loop, Sec. 3.4), against the oracle's run stored by
+    # tests/golden/make_oracle_golden.py: every step's counts, E^e, the next
+    # p_r, H_l after each epoch, and held-out early-exit counts (Sec. 3.1).
+    import hashlib
+    import json
+    import os
+    torch = torch_cuda()
+    from paper_2412_00119_amd.bmlp import BMLP
+    gold = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "small_five_epochs.json")))
+    w = synth.SMALL
+    assert (tuple(gold["widths"]), gold["batch"], gold["bound"]) == (w.widths, w.batch, w.bound)
+    net = BMLP(w.widths, w.n_classes, w.bound, 1000, w.group_size, w.robustness, w.seed_model)
+    tr = synth.make_split(w, "train")
+    te = synth.make_split(w, "test")
+    xb = net.pack(torch.from_numpy(tr.x).cuda())
+    yt = torch.from_numpy(tr.y.astype(np.int32)).cuda()
+    xe = net.pack(torch.from_numpy(te.x).cuda())
+    ye = torch.from_numpy(te.y.astype(np.int32)).cuda()
+    cfg = ob.Config(w.widths, w.n_classes, w.bound, w.group_size, w.robustness, w.seed_model)
+    P0 = [ob.init_layer(cfg, l)[1] for l in range(1, w.n_layers + 1)]
+    p_r, t = w.p_r, 0
+    for ep in gold["epochs"]:
+        e = ep["epoch"]
+        assert ep["step0"] == t and float.fromhex(ep["p_r"]) == p_r
+        order = torch.from_numpy(synth.epoch_order(w, e, len(tr.y)).astype(np.int32)).cuda()
+        p_next, err_frac, counts = net.train_epoch(xb, yt, order, t, p_r, batch=w.batch)
+        np.testing.assert_array_equal(counts.numpy(), np.asarray(ep["stats"]), err_msg=f"epoch {e} step counts")
+        assert err_frac == float.fromhex(ep["error_fraction"]), (e, err_frac)
+        assert p_next == float.fromhex(ep["p_r_next"]), (e, p_next)
+        for l in range(1, w.n_layers + 1):
+            h = net.H(l).cpu().numpy()
+            assert hashlib.sha256(h.tobytes()).hexdigest() == ep["h_sha256"][l - 1], f"epoch {e} H_{l}"
+            Wg = net.W(l).cpu().numpy().view(np.uint64)
+            np.testing.assert_array_equal(Wg, pack_np(np.where(h > 0, 1, -1).astype(np.int8), Wg.shape[1]),
+                                          err_msg=f"epoch {e} W_{l} = sign(H_{l})")
+            Pg = net.P(l).cpu().numpy().view(np.uint64)
+            np.testing.assert_array_equal(Pg, pack_np(P0[l - 1], Pg.shape[1]), err_msg=f"epoch {e} P_{l}")
+        exits = None
+        for s in range(0, len(te.y), 1000):
+            exits = net.eval_exit(xe[s:s + 1000], ye[s:s + 1000], exits)
+        exits = exits.cpu().numpy()
+        np.testing.assert_array_equal(exits, np.asarray(ep["heldout_exit_counts"]), err_msg=f"epoch {e} exits")
+        note(f"epoch {e}: E = {err_frac:.5f}, p_r -> {p_next:.6f}, held-out correct per layer "
+             f"{exits[:, 0].tolist()} of {len(te.y)}, exits {exits[:, 1].tolist()}")
+        t += counts.shape[0]
+        p_r = p_next
