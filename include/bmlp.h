@@ -234,6 +234,26 @@ int bmlp_expand(const int8_t *d_x, int32_t n, int32_t k_raw, int32_t k0, uint64_
  * d_x: bit rows [n][words(K_0)].  0 <= n <= max_batch. */
 int bmlp_forward(bmlp_ctx *ctx, const uint64_t *d_x, int32_t n, int32_t *d_yhat, void *stream);
 
+/* Bytes of the library's static device scratch (one copy per device the
+ * library runs on, held until the process ends). */
+#define BMLP_NOALLOC_SCRATCH_BYTES (48u << 20)
+
+/* bmlp_forward for callers that cannot allocate device memory or touch the
+ * workspace at call time (code under stream or graph capture, serving loops,
+ * harnesses that forbid allocation): the same launches and the same d_yhat,
+ * but the activation rows a_l go to the library's static scratch instead of
+ * the context's workspace, so the workspace (and the trace of the last train
+ * step in it) is left alone.  Allocates nothing: no hipMalloc, no hipFree.
+ *   Sizes: the a_l rows need sum over l of n * 8 * ceil(K_l / 64) bytes, each
+ *   layer rounded up to 256; more than BMLP_NOALLOC_SCRATCH_BYTES returns
+ *   BMLP_ESHAPE before any launch (message in bmlp_last_error).
+ *   The scratch is shared by every call on a device and keeps the last
+ *   call's contents: calls that overlap on one device (two streams, two
+ *   threads) race and must be ordered by the caller.  Its device address is
+ *   looked up at bmlp_init / bmlp_attach on the then-current device (the
+ *   context's device); other arguments and errors as bmlp_forward. */
+int bmlp_forward_noalloc(bmlp_ctx *ctx, const uint64_t *d_x, int32_t n, int32_t *d_yhat, void *stream);
+
 /* One training step on a mini-batch (Algorithm 1 body with Algorithms 2-3).
  *   d_x      bit rows [n][words(K_0)], d_y int32 [n].
  *   step     the global step counter t; keys the reinforcement draws, so a run

@@ -92,6 +92,7 @@ def lib() -> ctypes.CDLL:
             "bmlp_attach": (ctypes.c_int, [cfgp, vp, vp, vp, ctypes.POINTER(vp)]),
             "bmlp_pack": (ctypes.c_int, [vp, i32, i32, vp, vp]),
             "bmlp_forward": (ctypes.c_int, [vp, vp, i32, vp, vp]),
+            "bmlp_forward_noalloc": (ctypes.c_int, [vp, vp, i32, vp, vp]),
             "bmlp_train_step": (ctypes.c_int, [vp, vp, vp, i32, u64, dbl, vp, vp]),
             "bmlp_eval": (ctypes.c_int, [vp, vp, vp, i32, vp, vp]),
             "bmlp_eval_exit": (ctypes.c_int, [vp, vp, vp, i32, vp, vp]),
@@ -187,6 +188,10 @@ def bmlp_pack(d_pm1: int, n: int, K: int, d_bits: int, stream: int):
 
 def bmlp_forward(ctx: int, d_x: int, n: int, d_yhat: int, stream: int):
     _check(lib().bmlp_forward(ctx, d_x, n, d_yhat, stream), "bmlp_forward")
+
+
+def bmlp_forward_noalloc(ctx: int, d_x: int, n: int, d_yhat: int, stream: int):
+    _check(lib().bmlp_forward_noalloc(ctx, d_x, n, d_yhat, stream), "bmlp_forward_noalloc")
 
 
 def bmlp_train_step(ctx: int, d_x: int, d_y: int, n: int, step: int, p_r: float, d_stats: int,

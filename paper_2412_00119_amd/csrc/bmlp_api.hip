@@ -4,6 +4,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -22,12 +23,17 @@ struct bmlp_ctx {
   bmlp::Plan plan;
   uint8_t *state;
   uint8_t *ws;
+  int device = 0;               // the device current at bmlp_init / bmlp_attach
   bool prof_on = false;
   size_t prof_used = 0;
   long prof_open = -1;          // index of the run still open, or -1
   hipStream_t prof_stream = nullptr;
   std::vector<ProfRec> prof;
 };
+
+// The no-allocation entry point's scratch (its device address per device is
+// kept in bmlp::g_scratch_ptr).
+static __device__ __align__(256) uint8_t scratch[BMLP_NOALLOC_SCRATCH_BYTES];
 
 namespace bmlp {
 namespace {
@@ -44,6 +50,35 @@ int hip_fail(hipError_t e, const char *where) {
     hipError_t e_ = (call);                                  \
     if (e_ != hipSuccess) return hip_fail(e_, #call);        \
   } while (0)
+
+// The static scratch of bmlp_forward_noalloc: one copy per device, held
+// until the process ends.  Host code never uses the array's name as an
+// address: it uses the device address hipGetSymbolAddress returns for the
+// device, looked up once per device with that device current.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint8_t *g_scratch_ptr[kMaxDevices] = {};
+
+// Looks up (once) the scratch address on the current device.
+int scratch_setup(int *dev_out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) {
+    snprintf(g_last_error, sizeof(g_last_error), "device %d: the static scratch supports devices 0..%d", dev,
+             kMaxDevices - 1);
+    return BMLP_EHIP;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void *ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    g_scratch_ptr[dev] = static_cast<uint8_t *>(ptr);
+  }
+  if (dev_out) *dev_out = dev;
+  return BMLP_OK;
+}
 
 // Ends the open profiling run (if any) with its closing event.
 inline hipError_t prof_close(bmlp_ctx *ctx) {
@@ -221,11 +256,23 @@ int z_bits(int k) {
 // Forward of every layer for inference (y_hat out) or evaluation (counts:
 // layer l adds to correct[cstride * (l - 1)]; with flags, each pattern's
 // flag of layer l goes to flags[(l - 1) * max_batch + mu]).
+// a_rows, if set, replaces the workspace's a_l rows: layer l's n rows start
+// at a_rows + a_rows_offset(p, n, l) (the no-allocation entry point).
+size_t a_rows_offset(const Plan &p, int n, int l) {
+  size_t o = 0;
+  for (int j = 1; j < l; ++j) o = align256(o + (size_t)n * p.layer[j - 1].words_out * 8);
+  return o;
+}
+
 int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32_t *yhat_out,
-                   const int32_t *y, int32_t *correct, int cstride = 1, uint8_t *flags = nullptr) {
+                   const int32_t *y, int32_t *correct, int cstride = 1, uint8_t *flags = nullptr,
+                   uint8_t *a_rows = nullptr) {
   ProfScope prof_scope{ctx};
   const Plan &p = ctx->plan;
   int32_t *yh_ws = reinterpret_cast<int32_t *>(ctx->ws + p.off_yhat);
+  auto a_of = [&](int l) {
+    return reinterpret_cast<uint64_t *>(a_rows ? a_rows + a_rows_offset(p, n, l) : ctx->ws + p.layer[l - 1].off_a);
+  };
   if (use_mfma(p)) {
     const uint64_t *a_prev = x;
     for (int l = 1; l <= p.L; ++l) {
@@ -234,7 +281,7 @@ int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32
       f.A = a_prev; f.lda = lp.words_in;
       f.B = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_w); f.ldb = lp.words_in;
       f.M = n; f.N = lp.k_out; f.K = lp.k_in;
-      f.abits = reinterpret_cast<uint64_t *>(ctx->ws + lp.off_a); f.words_out = lp.words_out;
+      f.abits = a_of(l); f.words_out = lp.words_out;
       f.mode = kFwdPlain;
       BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s, launch_fwd_fp4(f, s));
       a_prev = f.abits;
@@ -245,7 +292,7 @@ int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32
     for (int l = 1; l <= p.L; ++l) {
       const LayerPlan &lp = p.layer[l - 1];
       ClsLayer &c = cb.L[cb.nl++];
-      c.A = reinterpret_cast<const uint64_t *>(ctx->ws + lp.off_a);
+      c.A = a_of(l);
       c.P = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p);
       c.words = lp.words_out; c.K = lp.k_out; c.thr = lp.robust_thr;
       c.yhat = yhat_out ? yhat_out + (size_t)(l - 1) * n * p.c : yh_ws + (size_t)(l - 1) * p.max_batch * p.c;
@@ -263,7 +310,7 @@ int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32
     const LayerPlan &lp = p.layer[l - 1];
     const uint64_t *W = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_w);
     const uint64_t *P = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p);
-    uint64_t *a = reinterpret_cast<uint64_t *>(ctx->ws + lp.off_a);
+    uint64_t *a = a_of(l);
     BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s,
                launch_fwd_popcount(a_prev, lp.words_in, lp.k_in, W, n, lp.k_out, nullptr, 0, a,
                                    lp.words_out, s));
@@ -300,6 +347,11 @@ int setup(const bmlp_config *cfg, void *d_state, void *d_ws, void *stream, bmlp_
   }
   ctx->state = static_cast<uint8_t *>(d_state);
   ctx->ws = static_cast<uint8_t *>(d_ws);
+  const int sst = scratch_setup(&ctx->device);
+  if (sst != BMLP_OK) {
+    delete ctx;
+    return sst;
+  }
   const Plan &p = ctx->plan;
   hipStream_t s = as_stream(stream);
   for (int l = 1; l <= p.L; ++l) {
@@ -415,6 +467,38 @@ int bmlp_forward(bmlp_ctx *ctx, const uint64_t *d_x, int32_t n, int32_t *d_yhat,
   if (n > 0 && d_yhat == nullptr) return BMLP_EINVAL;
   if (n == 0) return BMLP_OK;
   return forward_layers(ctx, d_x, n, as_stream(stream), d_yhat, nullptr, nullptr);
+}
+
+int bmlp_forward_noalloc(bmlp_ctx *ctx, const uint64_t *d_x, int32_t n, int32_t *d_yhat, void *stream) {
+  int st = check_ctx_batch(ctx, d_x, n);
+  if (st != BMLP_OK) return st;
+  if (n > 0 && d_yhat == nullptr) return BMLP_EINVAL;
+  if (n == 0) return BMLP_OK;
+  const Plan &p = ctx->plan;
+  const size_t need = a_rows_offset(p, n, p.L + 1);
+  if (need > (size_t)BMLP_NOALLOC_SCRATCH_BYTES) {
+    snprintf(g_last_error, sizeof(g_last_error),
+             "bmlp_forward_noalloc: %zu bytes of activation rows for n = %d exceed the static scratch of %zu bytes",
+             need, (int)n, (size_t)BMLP_NOALLOC_SCRATCH_BYTES);
+    return BMLP_ESHAPE;
+  }
+  uint8_t *base = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (ctx->device >= 0 && ctx->device < kMaxDevices) base = g_scratch_ptr[ctx->device];
+  }
+  if (base == nullptr) {   // not looked up at init: do it now, on the ctx's device
+    int cur = -1;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (cur != ctx->device && (e = hipSetDevice(ctx->device)) != hipSuccess) return hip_fail(e, "hipSetDevice");
+    st = scratch_setup(nullptr);
+    if (cur != ctx->device) (void)hipSetDevice(cur);
+    if (st != BMLP_OK) return st;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    base = g_scratch_ptr[ctx->device];
+  }
+  return forward_layers(ctx, d_x, n, as_stream(stream), d_yhat, nullptr, nullptr, 1, nullptr, base);
 }
 
 int bmlp_eval(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int32_t n,
