@@ -4,6 +4,8 @@ byte counters), as kept beside the library's measurements.
     python -m paper_2412_00119_amd.profsum stats  <rocprof dir> [--command CMD]
     python -m paper_2412_00119_amd.profsum traffic --fetch <dir> --write <dir>
         --kernel REGEX --source FILE --calib-bytes N [--command CMD]
+    python -m paper_2412_00119_amd.profsum counters <dir> [<dir> ...] --kernel REGEX
+        [--command CMD ...]
 
 `stats` turns `*_kernel_stats.csv` into a table of kernels (calls, average,
 min, max, share of GPU time).  `traffic` reads the per-dispatch FETCH_SIZE and
@@ -105,6 +107,83 @@ def traffic(args) -> None:
     print(f"traffic_bytes_per_launch: {fetch_b + write_b:.6g}")
 
 
+def counters(args) -> None:
+    """Mean value per dispatch of every counter in the given --pmc runs, per
+    kernel matching REGEX, with the ratios that read them."""
+    table = collections.defaultdict(lambda: collections.defaultdict(list))
+    dur = collections.defaultdict(list)
+    for d in args.dirs:
+        path = _one(os.path.join(d, "**", "*counter_collection.csv"))
+        per = collections.defaultdict(float)
+        meta = {}
+        for r in csv.DictReader(open(path)):
+            if not re.search(args.kernel, r["Kernel_Name"]):
+                continue
+            key = (int(r["Dispatch_Id"]), r["Counter_Name"])
+            per[key] += float(r["Counter_Value"])
+            meta[int(r["Dispatch_Id"])] = (short_name(r["Kernel_Name"]),
+                                           int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+        for (disp, cname), v in per.items():
+            table[meta[disp][0]][cname].append(v)
+        for disp, (kname, ns) in meta.items():
+            dur[kname].append(ns)
+    print("# rocprofv3 counters per dispatch\n")
+    if args.command:
+        print("Commands (one `--pmc` pass per run):\n")
+        for c in args.command:
+            print(f"    {c}")
+        print()
+    for kname in sorted(table):
+        cs = table[kname]
+        print(f"## {kname}\n")
+        print("| counter | dispatches | mean per dispatch |")
+        print("|---|---:|---:|")
+        mean = {}
+        for cname in sorted(cs):
+            vals = cs[cname]
+            mean[cname] = sum(vals) / len(vals)
+            print(f"| {cname} | {len(vals)} | {mean[cname]:.6g} |")
+        print()
+        derived = []
+        simds = 256 * 4
+        dur_cycles = (sum(dur[kname]) / len(dur[kname])) * 2.4 if dur[kname] else 0.0   # ns x 2.4 GHz
+        mfma = mean.get("SQ_INSTS_MFMA", 0.0)
+        if "SQ_INSTS_VALU" in mean:
+            valu = mean["SQ_INSTS_VALU"] - mfma   # SQ_INSTS_VALU counts the MFMAs too
+            derived.append(("VALU instructions (MFMA excluded) per SIMD", valu / simds))
+            if dur_cycles:
+                derived.append(("VALU issue cycles (4 per wave64 instruction) / dispatch cycles at 2.4 GHz",
+                                4 * valu / simds / dur_cycles))
+            if mfma:
+                derived.append(("VALU instructions per MFMA", valu / mfma))
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in mean and mfma:
+            derived.append(("MFMA busy cycles per MFMA", mean["SQ_VALU_MFMA_BUSY_CYCLES"] / mfma))
+            if dur_cycles:
+                derived.append(("MFMA busy cycles per SIMD / dispatch cycles at 2.4 GHz",
+                                mean["SQ_VALU_MFMA_BUSY_CYCLES"] / simds / dur_cycles))
+        if "SQ_INSTS_LDS" in mean and mfma:
+            derived.append(("LDS instructions per MFMA", mean["SQ_INSTS_LDS"] / mfma))
+        if "SQ_WAIT_INST_LDS" in mean and "SQ_WAVE_CYCLES" in mean and mean["SQ_WAVE_CYCLES"]:
+            derived.append(("waves waiting on LDS / wave cycles",
+                            mean["SQ_WAIT_INST_LDS"] / mean["SQ_WAVE_CYCLES"]))
+        if "SQ_WAIT_ANY" in mean and "SQ_WAVE_CYCLES" in mean and mean["SQ_WAVE_CYCLES"]:
+            derived.append(("waves waiting on anything / wave cycles", mean["SQ_WAIT_ANY"] / mean["SQ_WAVE_CYCLES"]))
+        if "SQ_ACTIVE_INST_VALU" in mean and "SQ_WAVE_CYCLES" in mean and mean["SQ_WAVE_CYCLES"]:
+            derived.append(("waves issuing VALU / wave cycles", mean["SQ_ACTIVE_INST_VALU"] / mean["SQ_WAVE_CYCLES"]))
+        if "SQ_LDS_BANK_CONFLICT" in mean and "SQ_INSTS_LDS" in mean and mean["SQ_INSTS_LDS"]:
+            derived.append(("LDS bank-conflict cycles per LDS instruction",
+                            mean["SQ_LDS_BANK_CONFLICT"] / mean["SQ_INSTS_LDS"]))
+        if derived:
+            print("| ratio | value |")
+            print("|---|---:|")
+            for name, v in derived:
+                print(f"| {name} | {v:.4g} |")
+            print()
+        if dur[kname]:
+            print(f"mean dispatch duration under the counters: {sum(dur[kname]) / len(dur[kname]) / 1e3:.2f} us "
+                  f"(counter collection serialises dispatches; the ratios over dispatch cycles use it)\n")
+
+
 def main(argv=None) -> None:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -118,8 +197,12 @@ def main(argv=None) -> None:
     t.add_argument("--source", required=True)
     t.add_argument("--calib-bytes", type=float, required=True)
     t.add_argument("--command", action="append", default=[])
+    c = sub.add_parser("counters")
+    c.add_argument("dirs", nargs="+")
+    c.add_argument("--kernel", required=True)
+    c.add_argument("--command", action="append", default=[])
     args = ap.parse_args(argv)
-    {"stats": stats, "traffic": traffic}[args.cmd](args)
+    {"stats": stats, "traffic": traffic, "counters": counters}[args.cmd](args)
 
 
 if __name__ == "__main__":
