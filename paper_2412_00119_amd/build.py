@@ -19,13 +19,15 @@ LIB_NAME = "libbmlp.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
 ARCH = "gfx950"
 
-HIP_FLAGS = [
-    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
-    "-ffp-contract=off",
-    # keep packed-fp32 instructions out of device code
-    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    "-Wall", "-Wno-unused-function",
-]
+COMMON_FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=off",
+                "-Wall", "-Wno-unused-function"]
+# Device pass only: keep packed-fp32 instructions out of device code.  The
+# host pass would not know the feature, so each source is compiled twice,
+# device code first, then the host code with that device code embedded, under
+# one compilation-unit id so that both passes name static device variables
+# alike.
+DEVICE_FLAGS = ["--offload-device-only", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+HOST_FLAGS = ["--offload-host-only"]
 
 
 def hipcc() -> str:
@@ -39,16 +41,49 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def build(verbose: bool = False) -> str:
-    """Compile libbmlp.so; returns its path.  Raises on a compile error."""
-    tmp = LIB_PATH + ".tmp"
-    cmd = [hipcc(), *HIP_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", *sources(), "-o", tmp]
+def host_sources():
+    """Plain C++ sources (the host planning code): compiled for the host only."""
+    return sorted(glob.glob(os.path.join(CSRC, "*.cpp")))
+
+
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError(f"hipcc failed ({res.returncode})")
+        raise RuntimeError(f"hipcc failed ({res.returncode}): {' '.join(cmd)}")
+    if res.stderr.strip():
+        sys.stderr.write(res.stderr)
+
+
+def _compile(src: str, objdir: str, verbose: bool) -> str:
+    name = os.path.splitext(os.path.basename(src))[0]
+    if src.endswith(".cpp"):
+        obj = os.path.join(objdir, name + ".o")
+        _run([hipcc(), "-x", "c++", "-O3", "-std=c++17", "-fPIC", "-Wall", f"-I{INCLUDE}", f"-I{CSRC}",
+              "-c", src, "-o", obj], verbose)
+        return obj
+    inc = [f"-I{INCLUDE}", f"-I{CSRC}", f"-cuid=bmlp_{name}"]
+    dev = os.path.join(objdir, name + ".dev")
+    obj = os.path.join(objdir, name + ".o")
+    _run([hipcc(), *COMMON_FLAGS, *DEVICE_FLAGS, *inc, "-c", src, "-o", dev], verbose)
+    _run([hipcc(), *COMMON_FLAGS, *HOST_FLAGS, *inc, "-Xclang", "-fcuda-include-gpubinary", "-Xclang", dev,
+          "-c", src, "-o", obj], verbose)
+    return obj
+
+
+def build(verbose: bool = False) -> str:
+    """Compile libbmlp.so; returns its path.  Raises on a compile error."""
+    import concurrent.futures
+    import tempfile
+    with tempfile.TemporaryDirectory(prefix="bmlp_build_") as objdir:
+        srcs = sources() + host_sources()
+        workers = max(1, min(len(srcs), len(os.sched_getaffinity(0)), 16))
+        with concurrent.futures.ThreadPoolExecutor(workers) as pool:
+            objs = list(pool.map(lambda f: _compile(f, objdir, verbose), srcs))
+        tmp = LIB_PATH + ".tmp"
+        _run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
     os.replace(tmp, LIB_PATH)
     return LIB_PATH
 

@@ -6,6 +6,7 @@
 #include <stdint.h>
 
 #include "bmlp.h"
+#include "plan.h"
 
 namespace bmlp {
 
@@ -17,38 +18,6 @@ enum : uint32_t {
   kStreamFine = 4,      // reinforcement: low 24 bits of the 32-bit draw
   kStreamGroups = 6,    // per-step group order (reshuffle variant)
 };
-
-// Bit planes of H: u = (h + B) / 2 lies in [0, B], B odd.
-__host__ __device__ inline int h_planes(int bound) {
-  int m = 1;
-  while ((1 << m) <= bound) ++m;
-  return m;
-}
-
-struct LayerPlan {
-  int k_in, k_out, gamma, groups;
-  int words_in, words_out;   // uint64 words per bit row of a_{l-1} / a_l
-  int ld_h;                  // bytes per H row: h_planes planes of h_ps words
-  int h_ps;                  // 32-bit words per plane of an H row, multiple of 16
-  int robust_thr;            // ceil(r K_l)
-  size_t off_h, off_w, off_p;                              // state
-  size_t off_a, off_err, off_upd, off_kstar, off_perm;     // workspace
-};
-
-struct Plan {
-  int L, c, max_batch, bound, fwd_impl, variants;
-  double r;
-  uint64_t seed;
-  int widths[BMLP_MAX_LAYERS + 1];
-  LayerPlan layer[BMLP_MAX_LAYERS];   // layer[l-1] describes layer l
-  int ldz;                            // int16 elements per row of the z scratch
-  size_t off_z, off_yhat;             // shared scratch in the workspace
-  size_t off_flag, off_xb, off_yb;    // early-exit flags; a gathered batch (epoch driver)
-  size_t state_bytes, ws_bytes;
-};
-
-// Validates cfg and fills plan; returns a BMLP_* status.
-int make_plan(const bmlp_config *cfg, Plan *plan);
 
 // ---------------------------------------------------------------------------
 // Launchers (each returns hipSuccess or the launch error).
