@@ -217,22 +217,35 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
       }
     }
   };
-  // MFMA K block (c, q): dword q of the lane's 16 bytes of chunk c
-  auto compute = [&](const Ops &o) {
+  // The expanded operands of one K block (c, q) of a step.  A step's MFMAs
+  // take block 0 expanded beforehand (by the step before, or the prologue);
+  // while the MFMAs of block b run, the operands of block b + 1 are expanded,
+  // and during the last block those of block 0 of the next step, so that the
+  // matrix core never waits for an expansion at the start of a step.
+  struct Exp {
+    uint4 a[2], b[2];
+  };
+  auto expand = [&](const Ops &o, int c, int q, Exp &e) {
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+    for (int i = 0; i < 2; ++i) e.a[i] = fp4x32_permuted(dword(o.a[c][i], q));
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        uint4 ea[2], eb[2];
+    for (int j = 0; j < 2; ++j) e.b[j] = fp4x32_permuted(dword(o.b[c][j], q));
+  };
+  auto compute_pipe = [&](const Ops &o, const Exp &e0, const Ops &onext, Exp &e0next) {
+    Exp e = e0;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) ea[i] = fp4x32_permuted(dword(o.a[c][i], q));
+    for (int blk = 0; blk < 8; ++blk) {
+      Exp en;
+      if (blk < 7)
+        expand(o, (blk + 1) >> 2, (blk + 1) & 3, en);
+      else
+        expand(onext, 0, 0, e0next);
 #pragma unroll
-        for (int j = 0; j < 2; ++j) eb[j] = fp4x32_permuted(dword(o.b[c][j], q));
+      for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-          for (int j = 0; j < 2; ++j) acc[i][j] = mfma_fp4(ea[i], eb[j], acc[i][j]);
-      }
+        for (int j = 0; j < 2; ++j) acc[i][j] = mfma_fp4(e.a[i], e.b[j], acc[i][j]);
+      if (blk < 7) e = en;
+    }
   };
   // the last step when K is not a multiple of 512: elements past K become
   // fp4 zeros in the W_l operand
@@ -283,12 +296,14 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   wait_vm<kIssue * (kStages - 2)>();   // this wave's loads of step 0 (and wave 0's labels) are done
   __builtin_amdgcn_s_barrier();        // every wave's loads of step 0 have landed
   read(r0, s0);
+  Exp e0, e1;
+  expand(r0, 0, 0, e0);
   const int yl = min(max(sY[pr], 0), p.c - 1);   // stay inside P on a bad label
   const uint64_t prow = p.P[(size_t)yl * p.ldp + min(pwg, p.pw_max)];
   __builtin_amdgcn_sched_barrier(0);
   // The sched_barrier(0) fences pin the order of the phases; otherwise the
   // scheduler sinks the read-ahead to its use and the LDS latency reappears.
-  auto step = [&](int ks, Ops &cur, Ops &nxt, const uint8_t *rs, uint8_t *ds) {
+  auto step = [&](int ks, Ops &cur, Ops &nxt, const Exp &ecur, Exp &enxt, const uint8_t *rs, uint8_t *ds) {
     __builtin_amdgcn_sched_barrier(0);
     wait_vm<kIssue * (kStages - 3)>();   // step ks+1 landed; ks+2 may still be in flight
     // A plain s_barrier: the fence of __syncthreads would also wait for the
@@ -296,32 +311,36 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     __builtin_amdgcn_s_barrier();
     issue(min(ks + kStages - 1, klast), ds);
     __builtin_amdgcn_sched_barrier(0);
-    compute(cur);
     read(nxt, rs);   // past the last step this reads a slot nobody uses
-    // one LDS read after each of the first MFMAs (issued before them, the
-    // reads would share the wait-count of the operands being consumed)
+    compute_pipe(cur, ecur, nxt, enxt);
+    // The order of the step's instructions: each MFMA followed by a seventh
+    // of the next K block's expansion, so that the VALU work runs while the
+    // matrix core works on the MFMA; one LDS read after each of the first
+    // eight MFMAs (issued before them, the reads would share the wait-count
+    // of the operands being consumed).
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < 32; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+      if (i < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+      __builtin_amdgcn_sched_group_barrier(0x002, 7, 0);   // VALU
     }
     __builtin_amdgcn_sched_barrier(0);
   };
   // step ks reads slot (ks+1) % 4 and refills slot (ks+3) % 4
   int ks = 0;
   for (; ks + kStages <= nfull; ks += kStages) {
-    step(ks + 0, r0, r1, s1, s3);
-    step(ks + 1, r1, r0, s2, s0);
-    step(ks + 2, r0, r1, s3, s1);
-    step(ks + 3, r1, r0, s0, s2);
+    step(ks + 0, r0, r1, e0, e1, s1, s3);
+    step(ks + 1, r1, r0, e1, e0, s2, s0);
+    step(ks + 2, r0, r1, e0, e1, s3, s1);
+    step(ks + 3, r1, r0, e1, e0, s0, s2);
   }
   // the last nfull % 4 full steps; r0 then holds the next step's operands
   if (ks < nfull) {
-    step(ks + 0, r0, r1, s1, s3);
+    step(ks + 0, r0, r1, e0, e1, s1, s3);
     if (ks + 1 < nfull) {
-      step(ks + 1, r1, r0, s2, s0);
+      step(ks + 1, r1, r0, e1, e0, s2, s0);
       if (ks + 2 < nfull) {
-        step(ks + 2, r0, r1, s3, s1);
+        step(ks + 2, r0, r1, e0, e1, s3, s1);
         r0 = r1;
       }
     } else {
