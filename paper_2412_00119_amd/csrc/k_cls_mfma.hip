@@ -23,9 +23,9 @@
 // partials in LDS (over the staged chunk) and every thread then adds the KG
 // partials of its own y_hat entries, in a fixed order.
 //
-// Then each wave takes one pattern: first argmax (lowest class on ties), the
-// two largest values (tau = top1 - top2, 0 on a tie), err = (pred != y) and
-// upd = err or tau < ceil(r K_l).  When the classes fit one pass y_hat is
+// Then sixteen lanes take each pattern: first argmax (lowest class on
+// ties), the two largest values (tau = top1 - top2, 0 on a tie), err =
+// (pred != y) and upd = err or tau < ceil(r K_l).  When the classes fit one pass y_hat is
 // read from LDS; otherwise each pass goes through the y_hat buffer.
 #include <limits.h>
 
@@ -38,7 +38,7 @@ namespace {
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = 16;
+constexpr int kWaves = 8;
 
 __device__ __forceinline__ v4f mfma_fp4(const uint4 &a, const uint4 &b, v4f c) {
   const v8i av = {(int)a.x, (int)a.y, (int)a.z, (int)a.w, 0, 0, 0, 0};
@@ -61,6 +61,16 @@ __device__ __forceinline__ Top2 merge(Top2 a, Top2 b) {
   }
   r.v2 = max(min(a.v1, b.v1), max(a.v2, b.v2));   // second largest of the union
   return r;
+}
+
+// a lane's top-two as seen through DPP control CTRL (a partner in its row)
+template <int CTRL>
+__device__ __forceinline__ Top2 dpp_top2(const Top2 &t) {
+  Top2 o;
+  o.v1 = __builtin_amdgcn_update_dpp(0, t.v1, CTRL, 0xF, 0xF, false);
+  o.i1 = __builtin_amdgcn_update_dpp(0, t.i1, CTRL, 0xF, 0xF, false);
+  o.v2 = __builtin_amdgcn_update_dpp(0, t.v2, CTRL, 0xF, 0xF, false);
+  return o;
 }
 
 template <int CB>
@@ -201,42 +211,45 @@ __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
   }
   if (p.mode == kClsYhatOnly) return;
 
-  for (int r = wave; r < 16; r += kWaves) {
+  // Sixteen lanes per pattern (a DPP row): lane li scans classes li, li + 16,
+  // ... in order, then the row merges its lanes' top-two with four DPP
+  // exchanges (xor 1 and 2 within quads, then the half-row and row mirrors),
+  // after which every lane of the row holds the pattern's first argmax and
+  // its two largest values.  Waves 0..3 take the 16 patterns.
+  if (wave < 4) {
+    const int r = 4 * wave + (lane >> 4), li = lane & 15;
     const int mu = m0 + r;
-    if (mu >= p.n) break;
-    Top2 t{INT_MIN, INT_MAX, INT_MIN};
-    const int32_t *row = Lr.yhat + (size_t)mu * p.c;
-    for (int cl = lane; cl < p.c; cl += 64) {
-      const int v = one_pass ? red[0][r][cl] : row[cl];
-      if (v > t.v1) {
-        t.v2 = t.v1;
-        t.v1 = v;
-        t.i1 = cl;
-      } else if (v > t.v2) {
-        t.v2 = v;
+    if (mu < p.n) {
+      Top2 t{INT_MIN, INT_MAX, INT_MIN};
+      const int32_t *row = Lr.yhat + (size_t)mu * p.c;
+      for (int cl = li; cl < p.c; cl += 16) {
+        const int v = one_pass ? red[0][r][cl] : row[cl];
+        if (v > t.v1) {
+          t.v2 = t.v1;
+          t.v1 = v;
+          t.i1 = cl;
+        } else if (v > t.v2) {
+          t.v2 = v;
+        }
       }
-    }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-      Top2 o;
-      o.v1 = __shfl_xor(t.v1, off, 64);
-      o.i1 = __shfl_xor(t.i1, off, 64);
-      o.v2 = __shfl_xor(t.v2, off, 64);
-      t = merge(t, o);
-    }
-    const int label = p.y[mu];
-    if (lane == 0) {
-      if (p.mode == kClsEval) {
-        if (t.i1 == label) atomicAdd(&cnt[2], 1);
-        if (Lr.flag != nullptr)
-          Lr.flag[mu] = (uint8_t)((t.i1 == label ? 1 : 0) | ((t.v1 - t.v2) >= Lr.thr ? 2 : 0));
-      } else {
-        const bool err = t.i1 != label;
-        const bool upd = err || (t.v1 - t.v2) < Lr.thr;
-        Lr.err[mu] = err ? 1 : 0;
-        Lr.upd[mu] = upd ? 1 : 0;
-        if (err) atomicAdd(&cnt[0], 1);
-        if (upd) atomicAdd(&cnt[1], 1);
+      t = merge(t, dpp_top2<0xB1>(t));    // quad_perm [1,0,3,2]
+      t = merge(t, dpp_top2<0x4E>(t));    // quad_perm [2,3,0,1]
+      t = merge(t, dpp_top2<0x141>(t));   // row_half_mirror
+      t = merge(t, dpp_top2<0x140>(t));   // row_mirror
+      if (li == 0) {
+        const int label = p.y[mu];
+        if (p.mode == kClsEval) {
+          if (t.i1 == label) atomicAdd(&cnt[2], 1);
+          if (Lr.flag != nullptr)
+            Lr.flag[mu] = (uint8_t)((t.i1 == label ? 1 : 0) | ((t.v1 - t.v2) >= Lr.thr ? 2 : 0));
+        } else {
+          const bool err = t.i1 != label;
+          const bool upd = err || (t.v1 - t.v2) < Lr.thr;
+          Lr.err[mu] = err ? 1 : 0;
+          Lr.upd[mu] = upd ? 1 : 0;
+          if (err) atomicAdd(&cnt[0], 1);
+          if (upd) atomicAdd(&cnt[1], 1);
+        }
       }
     }
   }
