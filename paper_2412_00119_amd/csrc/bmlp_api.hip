@@ -125,6 +125,25 @@ inline hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s);
 
 bool use_mfma(const Plan &p) { return p.fwd_impl != BMLP_FWD_POPCOUNT; }
 
+// y_hat = a_l P_l^T of one layer by the forward kernel, for class counts
+// above what the classifier kernel takes: int32 rows [n][c] into y32, or
+// int16 rows [n][ldy16] into y16.
+FwdArgs cls_gemm_args(const Plan &p, int l, const uint64_t *a, const uint64_t *P, int n, int32_t *y32,
+                      int16_t *y16) {
+  const LayerPlan &lp = p.layer[l - 1];
+  FwdArgs g{};
+  g.A = a; g.lda = lp.words_out;
+  g.B = P; g.ldb = lp.words_out;
+  g.M = n; g.N = p.c; g.K = lp.k_out;
+  g.abits = nullptr; g.words_out = 0;
+  if (y32 != nullptr) {
+    g.mode = kFwdWriteZ32; g.z32 = y32; g.ldz = p.c;
+  } else {
+    g.mode = kFwdWriteZ; g.z = y16; g.ldz = p.ldy16;
+  }
+  return g;
+}
+
 // Forward of every layer for inference (y_hat out) or evaluation (counts:
 // layer l adds to correct[cstride * (l - 1)]; with flags, each pattern's
 // flag of layer l goes to flags[(l - 1) * max_batch + mu]).  a_rows, if set,
@@ -140,6 +159,8 @@ int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32
     return reinterpret_cast<uint64_t *>(a_rows ? a_rows + a_rows_offset(p, n, l) : ctx->ws + p.layer[l - 1].off_a);
   };
   if (use_mfma(p)) {
+    const bool cls_gemm = p.c > kClsMaxClasses;
+    int16_t *y16_ws = reinterpret_cast<int16_t *>(ctx->ws + p.off_yhat);
     const uint64_t *a_prev = x;
     for (int l = 1; l <= p.L; ++l) {
       const LayerPlan &lp = p.layer[l - 1];
@@ -151,21 +172,30 @@ int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32
       f.mode = kFwdPlain;
       BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s, launch_fwd_fp4(f, s));
       a_prev = f.abits;
+      if (cls_gemm) {   // y_hat of layer l while a_l is fresh in the caches
+        FwdArgs g = cls_gemm_args(p, l, a_prev, reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p), n,
+                                  correct ? nullptr : yhat_out + (size_t)(l - 1) * n * p.c,
+                                  y16_ws + (size_t)(l - 1) * p.max_batch * p.ldy16);
+        BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_fwd_fp4(g, s));
+      }
     }
-    // every layer's local classifier in one launch per kMaxClsLayers layers
+    if (cls_gemm && !correct) return BMLP_OK;   // y_hat is the output
+    // every layer's local classifier (or, after the products above, its
+    // error signal) in one launch per kMaxClsLayers layers
     ClsBatch cb{};
-    cb.n = n; cb.c = p.c; cb.y = y; cb.mode = correct ? kClsEval : kClsYhatOnly;
+    cb.n = n; cb.c = p.c; cb.y = y; cb.mode = correct ? kClsEval : kClsYhatOnly; cb.ldy = p.ldy16;
     for (int l = 1; l <= p.L; ++l) {
       const LayerPlan &lp = p.layer[l - 1];
       ClsLayer &c = cb.L[cb.nl++];
       c.A = a_of(l);
       c.P = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p);
       c.words = lp.words_out; c.K = lp.k_out; c.thr = lp.robust_thr;
-      c.yhat = yhat_out ? yhat_out + (size_t)(l - 1) * n * p.c : yh_ws + (size_t)(l - 1) * p.max_batch * p.c;
+      c.yhat = yhat_out ? yhat_out + (size_t)(l - 1) * n * p.c : nullptr;
+      c.y16 = y16_ws + (size_t)(l - 1) * p.max_batch * p.ldy16;
       c.correct = correct ? correct + (size_t)cstride * (l - 1) : nullptr;
       c.flag = flags ? flags + (size_t)(l - 1) * p.max_batch : nullptr;
       if (cb.nl == kMaxClsLayers || l == p.L) {
-        BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_cls_fp4(cb, s));
+        BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, cls_gemm ? launch_cls_argmax(cb, s) : launch_cls_fp4(cb, s));
         cb.nl = 0;
       }
     }
@@ -371,6 +401,8 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
   if (n == 0) return BMLP_OK;
   int16_t *z = reinterpret_cast<int16_t *>(ctx->ws + p.off_z);
   int32_t *yh = reinterpret_cast<int32_t *>(ctx->ws + p.off_yhat);
+  int16_t *y16 = reinterpret_cast<int16_t *>(ctx->ws + p.off_yhat);
+  const bool cls_gemm = mfma && p.c > kClsMaxClasses;
   const bool reshuffle = p.variants & BMLP_VARIANT_RESHUFFLE_GROUPS;
   if (reshuffle) {   // this step's group order of every layer
     PermBatch pb{};
@@ -435,6 +467,10 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
         ls.yhat = nullptr;
         BMLP_TIMED(ctx, BMLP_KERNEL_SELECT, s, launch_loss_select(ls, s));
       }
+      if (cls_gemm) {   // Algorithm 1's y_hat of layer l, while a_l is fresh in the caches
+        FwdArgs g = cls_gemm_args(p, l, a, P, n, nullptr, y16 + (size_t)(l - 1) * p.max_batch * p.ldy16);
+        BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_fwd_fp4(g, s));
+      }
     } else {
       BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s,
                  launch_fwd_popcount(a_prev, lp.words_in, lp.k_in, W, n, lp.k_out, z, p.ldz, a,
@@ -447,20 +483,22 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
     a_prev = a;
   }
   if (mfma) {
-    // Algorithm 1's local output, loss and robustness test for every layer, one launch per kMaxClsLayers layers
+    // Algorithm 1's local output (or, after the products above, the error
+    // signal from it), loss and robustness test for every layer, one launch
+    // per kMaxClsLayers layers
     ClsBatch cb{};
-    cb.n = n; cb.c = p.c; cb.y = d_y; cb.mode = kClsTrain;
+    cb.n = n; cb.c = p.c; cb.y = d_y; cb.mode = kClsTrain; cb.ldy = p.ldy16;
     for (int l = 1; l <= p.L; ++l) {
       const LayerPlan &lp = p.layer[l - 1];
       ClsLayer &c = cb.L[cb.nl++];
       c.A = reinterpret_cast<const uint64_t *>(ctx->ws + lp.off_a);
       c.P = reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p);
       c.words = lp.words_out; c.K = lp.k_out; c.thr = lp.robust_thr;
-      c.yhat = yh + (size_t)(l - 1) * p.max_batch * p.c;
+      c.y16 = y16 + (size_t)(l - 1) * p.max_batch * p.ldy16;
       c.err = ctx->ws + lp.off_err; c.upd = ctx->ws + lp.off_upd;
       c.stats = d_stats + BMLP_STATS_STRIDE * (l - 1);
       if (cb.nl == kMaxClsLayers || l == p.L) {
-        BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_cls_fp4(cb, s));
+        BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, cls_gemm ? launch_cls_argmax(cb, s) : launch_cls_fp4(cb, s));
         cb.nl = 0;
       }
     }

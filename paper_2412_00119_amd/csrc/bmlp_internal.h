@@ -49,7 +49,10 @@ hipError_t launch_cls_popcount(const uint64_t *a, int words, int k, const uint64
                                int c, int32_t *out, int ldo, hipStream_t s);
 
 // Forward on the matrix cores: bit-row operands expanded to fp4 in registers.
-enum { kFwdFusedSelect = 0, kFwdWriteZ = 1, kFwdPlain = 2 };
+// The same contraction gives the local classifier's y_hat = a_l P_l^T (A =
+// a_l, B = P_l) when the classes are too many for the classifier kernel
+// (kFwdWriteZ or kFwdWriteZ32, words_out = 0: no sign bits).
+enum { kFwdFusedSelect = 0, kFwdWriteZ = 1, kFwdPlain = 2, kFwdWriteZ32 = 3 };
 struct FwdArgs {
   const uint64_t *A; int lda;       // a_{l-1} bit rows [M][lda words]
   const uint64_t *B; int ldb;       // W_l bit rows [N][ldb words]
@@ -59,23 +62,28 @@ struct FwdArgs {
   int16_t *kstar; int ldk;          // kFwdFusedSelect (gamma = 64): raw selection [groups][ldk]
   const int32_t *y; int c;          // kFwdFusedSelect: labels [M] and class count
   const uint64_t *P; int ldp;       // kFwdFusedSelect: P_l rows [c][ldp], rho^{y^mu} = P_l[y^mu]
-  int16_t *z; int ldz;              // kFwdWriteZ
+  int16_t *z; int ldz;              // kFwdWriteZ: z int16 [M][ldz]
+  int32_t *z32;                     // kFwdWriteZ32: z int32 [M][ldz]
   float zlo, zhi;                   // kFwdFusedSelect: the selection clips z to [zlo, zhi]
   int32_t *zero; int nzero;         // if set: zeroed by the first work-group (step statistics)
-  int nt_m, nt_n, xcd_remap;        // set by the launcher
+  int nt_m, nt_n, xcd_remap;        // set by the launcher (xcd_remap: 1 = slices of B, 2 = of A)
   int pw_max, ystride;              // set by the launcher: last word of a P row; label stride
 };
 hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s);
 
 // Classifier on the matrix cores, then the local error signal, for up to
-// kMaxClsLayers layers in one launch (ceil(n / 16) work-groups per layer).
+// kMaxClsLayers layers in one launch (ceil(n / 16) work-groups per layer),
+// for up to kClsMaxClasses classes.  Above that, y_hat comes from the
+// forward kernel (kFwdWriteZ) and launch_cls_argmax takes the error signal
+// from it.
+constexpr int kClsMaxClasses = 128;
 enum { kClsTrain = 0, kClsYhatOnly = 1, kClsEval = 2 };
 struct ClsLayer {
   const uint64_t *A;                // a_l bit rows [n][words]
   const uint64_t *P;                // P_l bit rows [c][words]
   int words, K, thr;                // words = ceil(K / 64)
-  int32_t *yhat;                    // y_hat int32 [n][c]: output (kClsYhatOnly), or
-                                    // scratch when c needs several passes
+  int32_t *yhat;                    // y_hat int32 [n][c]: output (kClsYhatOnly)
+  const int16_t *y16;               // launch_cls_argmax: y_hat int16 [n][ldy]
   uint8_t *err, *upd;               // train
   int32_t *stats;                   // train: this layer's [4], adds [0] and [1]
   int32_t *correct;                 // eval: adds the correct count
@@ -86,8 +94,11 @@ struct ClsBatch {
   ClsLayer L[kMaxClsLayers];
   int nl, n, c, mode;
   const int32_t *y;
+  int ldy;                          // launch_cls_argmax: a multiple of 4, >= c
 };
 hipError_t launch_cls_fp4(const ClsBatch &a, hipStream_t s);
+// The local error signal (kClsTrain or kClsEval) from stored int16 y_hat rows.
+hipError_t launch_cls_argmax(const ClsBatch &a, hipStream_t s);
 
 // 01-loss, margin and M (when yhat is given), and the easiest wrong
 // perceptron of every group for every pattern (U_l is its restriction to the

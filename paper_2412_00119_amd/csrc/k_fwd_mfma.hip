@@ -27,9 +27,12 @@
 //     columns k of the group with delta_k = z_k rho^{y}_k < 0, the smallest
 //     |z_k|, lowest k on ties (key = |z| << 8 | k, min-reduced across lanes
 //     with a butterfly reduce-scatter, so each lane ends with one row);
-//   * for any other gamma, z as int16 for the generic selection kernel.
+//   * for any other gamma, z as int16 for the generic selection kernel;
+//   * for the local classifier of a layer with many classes (A = a_l, B =
+//     P_l), y_hat as int16 or int32, and no sign bits.
 // Work-groups are mapped so that each XCD (work-group id mod 8) works on
-// its own slice of W_l, which then stays in that XCD's L2.
+// its own slice of the larger operand (W_l in a hidden layer, a_l against
+// a classifier matrix), which then stays in that XCD's L2.
 #include <algorithm>
 #include <type_traits>
 
@@ -137,10 +140,14 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   int mt, nt;
   {
     const int b = blockIdx.x;
-    if (p.xcd_remap) {
+    if (p.xcd_remap == 1) {   // XCD x takes the x-th eighth of B's tiles
       const int x = b & 7, idx = b >> 3, per = p.nt_n >> 3;
       nt = x * per + idx / p.nt_m;
       mt = idx % p.nt_m;
+    } else if (p.xcd_remap == 2) {   // the x-th eighth of A's tiles
+      const int x = b & 7, idx = b >> 3, per = p.nt_m >> 3;
+      mt = x * per + idx / p.nt_n;
+      nt = idx % p.nt_n;
     } else {
       nt = b / p.nt_m;
       mt = b % p.nt_m;
@@ -456,7 +463,8 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
       const int m = m0 + rl;
       if (m < p.M) p.kstar[(size_t)g * p.ldk + m] = (v[0] >> 31) ? (int16_t)-1 : (int16_t)(v[0] & 0x3Fu);
     }
-  } else if (p.mode == kFwdWriteZ) {
+  } else if (p.mode == kFwdWriteZ || p.mode == kFwdWriteZ32) {
+    const bool wide = p.mode == kFwdWriteZ32;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -465,7 +473,13 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
         for (int e = 0; e < 16; ++e) {
           const int m = m0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
           const int col = n0 + wn * 64 + j * 32 + lc;
-          if (m < p.M && col < p.N) p.z[(size_t)m * p.ldz + col] = (int16_t)(int)acc[i][j][e];
+          if (m < p.M && col < p.N) {
+            const size_t o = (size_t)m * p.ldz + col;
+            if (wide)
+              p.z32[o] = (int)acc[i][j][e];
+            else
+              p.z[o] = (int16_t)(int)acc[i][j][e];
+          }
         }
   }
   wait_vm<0>();   // the repeated loads write LDS: they land before the wave ends
@@ -478,7 +492,16 @@ hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s) {
   if (a.K < 1 || a.N < 1 || a.lda < (a.K + 63) / 64 || a.ldb < (a.K + 63) / 64) return hipErrorInvalidValue;
   a.nt_m = (a.M + TM - 1) / TM;
   a.nt_n = (a.N + TN - 1) / TN;
-  a.xcd_remap = (a.nt_n % 8 == 0) ? 1 : 0;
+  // each XCD keeps its slice of the larger operand in its own L2 (W_l in a
+  // hidden layer; a_l when B is a narrow classifier matrix P_l)
+  if (a.nt_m % 8 == 0 && (double)a.M * a.lda > (double)a.N * a.ldb)
+    a.xcd_remap = 2;
+  else
+    a.xcd_remap = (a.nt_n % 8 == 0) ? 1 : 0;
+  if (a.words_out > 0 && a.abits == nullptr) return hipErrorInvalidValue;
+  if ((a.mode == kFwdWriteZ && a.z == nullptr) || (a.mode == kFwdWriteZ32 && a.z32 == nullptr) ||
+      ((a.mode == kFwdWriteZ || a.mode == kFwdWriteZ32) && a.ldz < a.N))
+    return hipErrorInvalidValue;
   if (a.mode == kFwdFusedSelect) {
     if (a.y == nullptr || a.P == nullptr || a.c < 1) return hipErrorInvalidValue;
     a.pw_max = a.words_out - 1;

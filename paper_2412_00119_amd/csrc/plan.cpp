@@ -6,6 +6,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
+
 namespace bmlp {
 
 // Group-size rule of Section 4.3: the divisor of K closest to any value of
@@ -106,8 +108,9 @@ int make_plan(const bmlp_config *cfg, Plan *p) {
   p->ldz = 64 * words64(kmax);
   p->off_z = wo;
   wo = align256(wo + (size_t)nb * p->ldz * 2);
-  p->off_yhat = wo;   // [L][max_batch][c]
-  wo = align256(wo + (size_t)p->L * nb * p->c * 4);
+  p->off_yhat = wo;   // int32 [L][max_batch][c], or int16 [L][max_batch][ldy16]
+  p->ldy16 = (p->c + 7) & ~7;
+  wo = align256(wo + (size_t)p->L * nb * std::max((size_t)p->c * 4, (size_t)p->ldy16 * 2));
   p->ws_bytes = wo;
   return BMLP_OK;
 }

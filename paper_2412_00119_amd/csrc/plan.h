@@ -36,6 +36,7 @@ struct Plan {
   LayerPlan layer[BMLP_MAX_LAYERS];   // layer[l-1] describes layer l
   int ldz;                            // int16 elements per row of the z scratch
   size_t off_z, off_yhat;             // shared scratch in the workspace
+  int ldy16;                          // y_hat as int16 rows [L][max_batch][ldy16] (in off_yhat)
   size_t off_flag, off_xb, off_yb;    // early-exit flags; a gathered batch (epoch driver)
   size_t state_bytes, ws_bytes;
 };

@@ -15,14 +15,15 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("fwd_impl", [1, 2])
-def test_forward_noalloc_matches_forward(fwd_impl):
+@pytest.mark.parametrize("c", [11, 300])   # 300: y_hat from the forward kernel, into the output
+def test_forward_noalloc_matches_forward(fwd_impl, c):
     torch = torch_cuda()
     from paper_2412_00119_amd import bmlp as B
-    widths, c = (200, 192, 130, 64), 11
+    widths = (200, 192, 130, 64)
     net = B.BMLP(widths, c, 15, 300, 0, 0.25, 11, fwd_impl)
     rng = np.random.default_rng(3)
     for n in (300, 77):
-        note(f"forward_noalloc impl {fwd_impl} n={n}")
+        note(f"forward_noalloc impl {fwd_impl} c={c} n={n}")
         xb = net.pack(torch.from_numpy(random_pm1((n, widths[0]), rng)).cuda())
         ref = torch.empty((net.n_layers, n, c), dtype=torch.int32, device="cuda")
         got = torch.full((net.n_layers, n, c), -7, dtype=torch.int32, device="cuda")
