@@ -141,63 +141,117 @@ __device__ __forceinline__ void add_count(uint32_t (&c)[kPlanes], const uint32_t
   }
 }
 
-// Loads the a-words of selectors s0 .. s0 + N - 1 of a row (list[beg + s]),
-// flipped where rho = -1, all loads in flight together; entries past S load a
-// valid word (the row's last selector) and become zero.
-template <int N>
-__device__ __forceinline__ void load_selectors(uint32_t (&x)[N], const uint16_t *list, int beg, int S, int s0,
-                                               const uint32_t *a32, int nw32, int cw) {
+// The a_{l-1} rows are read through a buffer descriptor: the selector's row
+// offset is a scalar (soffset) and the lane's word offset a vector register,
+// so a load costs no vector address arithmetic.  kRawRsrcWord3 is the fourth
+// descriptor word of a raw (stride 0) buffer of 32-bit words on this
+// architecture family.
+constexpr int kRawRsrcWord3 = 0x00020000;
+
+__device__ __forceinline__ uint32_t load_word(__amdgpu_buffer_rsrc_t rs, int voff, int soff) {
+  return __builtin_amdgcn_raw_buffer_load_b32(rs, voff, soff, 0);
+}
+
+// The 16 selector entries list[i .. i + 16) (i a multiple of 8, list 16-byte
+// aligned): two 16-byte LDS reads at an address every lane shares, moved to
+// scalar registers.
+__device__ __forceinline__ void read_entries16(const uint16_t *list, int i, uint32_t (&e)[8]) {
+  const uint4 a = *reinterpret_cast<const uint4 *>(list + i);
+  const uint4 b = *reinterpret_cast<const uint4 *>(list + i + 8);
+  e[0] = __builtin_amdgcn_readfirstlane(a.x);
+  e[1] = __builtin_amdgcn_readfirstlane(a.y);
+  e[2] = __builtin_amdgcn_readfirstlane(a.z);
+  e[3] = __builtin_amdgcn_readfirstlane(a.w);
+  e[4] = __builtin_amdgcn_readfirstlane(b.x);
+  e[5] = __builtin_amdgcn_readfirstlane(b.y);
+  e[6] = __builtin_amdgcn_readfirstlane(b.z);
+  e[7] = __builtin_amdgcn_readfirstlane(b.w);
+}
+
+// x[i] = a-word of entry i of e, flipped where rho = -1, for i < N; with
+// KEEP, entries i >= keep are zero (and read row 0, a valid address, since
+// the list slots past the row's selectors hold no entry).
+template <int N, bool KEEP>
+__device__ __forceinline__ void load_selectors(uint32_t (&x)[N], const uint32_t (&e)[8], int keep,
+                                               __amdgpu_buffer_rsrc_t rs, int rowbytes, int voff) {
 #pragma unroll
   for (int i = 0; i < N; ++i) {
-    const int s = s0 + i;
-    // every lane reads the same entry: make it a scalar
-    const uint32_t ent = __builtin_amdgcn_readfirstlane(list[beg + min(s, S - 1)]);
-    const uint32_t mu = ent & 0x7FFFu;
-    const uint32_t flip = (s < S) ? ((ent & 0x8000u) ? 0xFFFFFFFFu : 0u) : 0u;
-    const uint32_t keep = (s < S) ? 0xFFFFFFFFu : 0u;
-    x[i] = (a32[(size_t)mu * nw32 + cw] ^ flip) & keep;
+    const uint32_t ent = (e[i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+    const bool live = !KEEP || i < keep;
+    const int soff = live ? (int)(ent & 0x7FFFu) * rowbytes : 0;
+    const uint32_t flip = (ent & 0x8000u) ? 0xFFFFFFFFu : 0u;
+    const uint32_t w = load_word(rs, voff, soff) ^ flip;
+    x[i] = live ? w : 0u;
+  }
+}
+
+// c += n (NN planes) where the counters are at most `bound` afterwards: the
+// carry ripples only through the planes in use (a uniform exit, so c stays
+// in place).
+template <int NN>
+__device__ __forceinline__ void add_count_upto(uint32_t (&c)[kPlanes], const uint32_t (&n)[NN], int bound) {
+  const int np = 32 - __clz(bound);
+  uint32_t carry = 0u;
+#pragma unroll
+  for (int p = 0; p < kPlanes; ++p) {
+    if (p < NN) {
+      const uint32_t sum = c[p] ^ n[p] ^ carry;
+      carry = maj(c[p], n[p], carry);
+      c[p] = sum;
+    } else {
+      if (p >= np) break;
+      const uint32_t sum = c[p] ^ carry;
+      carry = c[p] & carry;
+      c[p] = sum;
+    }
   }
 }
 
 // Counts the +1 contributions of the row's S >= 1 selectors (list[beg ..
-// beg+S)) into bit-sliced counters: up to 8, or else the first 16, through a
-// carry-save tree, the rest 8 at a time added to the running count.
+// beg+S), beg a multiple of 8) into bit-sliced counters: batches of 16
+// through a carry-save tree, all 16 loads in flight together, each batch's
+// count added to the running one; the last batch (up to 15, or 8) masks
+// the slots past S.
 __device__ __forceinline__ void count_row(uint32_t (&c)[kPlanes], const uint16_t *list, int beg, int S,
-                                          const uint32_t *a32, int nw32, int cw) {
+                                          __amdgpu_buffer_rsrc_t rs, int rowbytes, int voff) {
 #pragma unroll
   for (int q = 0; q < kPlanes; ++q) c[q] = 0u;
-  if (S <= 8) {
-    uint32_t x[8], n[4];
-    load_selectors<8>(x, list, beg, S, 0, a32, nw32, cw);
-    compress8(x, n);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) c[q] = n[q];
-    return;
-  }
-  {
-    uint32_t x[16], n[5];
-    load_selectors<16>(x, list, beg, S, 0, a32, nw32, cw);
+  int s0 = 0;
+  for (; s0 + 16 <= S; s0 += 16) {
+    uint32_t e[8], x[16], n[5];
+    read_entries16(list, beg + s0, e);
+    load_selectors<16, false>(x, e, 16, rs, rowbytes, voff);
     compress16(x, n);
+    if (s0 == 0) {
 #pragma unroll
-    for (int q = 0; q < 5; ++q) c[q] = n[q];
+      for (int q = 0; q < 5; ++q) c[q] = n[q];
+    } else {
+      add_count_upto<5>(c, n, s0 + 16);
+    }
   }
-  for (int s0 = 16; s0 < S; s0 += 8) {
+  const int rem = S - s0;
+  if (rem == 0) return;
+  uint32_t e[8];
+  read_entries16(list, beg + s0, e);
+  if (rem <= 8) {
     uint32_t x[8], n[4];
-    load_selectors<8>(x, list, beg, S, s0, a32, nw32, cw);
+    load_selectors<8, true>(x, e, rem, rs, rowbytes, voff);
     compress8(x, n);
-    // planes in use after this batch: the counters are at most min(s0 + 8, S)
-    switch (32 - __clz(min(s0 + 8, S))) {
-      case 5: add_count<4, 5>(c, n); break;
-      case 6: add_count<4, 6>(c, n); break;
-      case 7: add_count<4, 7>(c, n); break;
-      case 8: add_count<4, 8>(c, n); break;
-      case 9: add_count<4, 9>(c, n); break;
-      case 10: add_count<4, 10>(c, n); break;
-      case 11: add_count<4, 11>(c, n); break;
-      case 12: add_count<4, 12>(c, n); break;
-      case 13: add_count<4, 13>(c, n); break;
-      case 14: add_count<4, 14>(c, n); break;
-      default: add_count<4, 15>(c, n); break;
+    if (s0 == 0) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) c[q] = n[q];
+    } else {
+      add_count_upto<4>(c, n, S);
+    }
+  } else {
+    uint32_t x[16], n[5];
+    load_selectors<16, true>(x, e, rem, rs, rowbytes, voff);
+    compress16(x, n);
+    if (s0 == 0) {
+#pragma unroll
+      for (int q = 0; q < 5; ++q) c[q] = n[q];
+    } else {
+      add_count_upto<5>(c, n, S);
     }
   }
 }
@@ -313,12 +367,19 @@ __device__ __forceinline__ uint32_t any_plane(const uint32_t (&u)[M]) {
   return e;
 }
 
+__device__ __host__ __forceinline__ int round8(int v) { return (v + 7) & ~7; }
+
+// Selector list slots: every row's selectors padded to a multiple of 8, and
+// 16 more so that a batch read of 16 entries stays inside the list; a
+// multiple of 8 slots, so that the bucket offsets after it stay aligned.
+__device__ __host__ __forceinline__ int list_slots(int n, int gamma) { return round8(n + 7 * gamma) + 16; }
+
 // FULL: B = 2^M - 1 (B = 1, 3, 7, 15, 31, 63, 127), so u = B is every plane
 // set and u >= (B + 1) / 2 is the top plane; otherwise the planar
 // comparisons with the constants of B.
 template <int M, bool FULL>
-__global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
-  extern __shared__ int smem[];
+__global__ __launch_bounds__(kThreads, kSplit * kWaves / 4) void update_kernel(UpdateBatch p) {
+  extern __shared__ __align__(16) int smem[];
   __shared__ int wsum[kWaves];
   __shared__ int s_sel;
 
@@ -335,8 +396,9 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   const int g = ((int)blockIdx.x - U.block0) / kSplit;
   const int part = ((int)blockIdx.x - U.block0) % kSplit;
   const int gamma = U.gamma;
-  int *bucket = smem;                                            // [gamma]
-  uint16_t *list = reinterpret_cast<uint16_t *>(smem + gamma);   // [n]
+  // the selector list first (16-byte aligned), then the bucket offsets
+  uint16_t *list = reinterpret_cast<uint16_t *>(smem);               // [list_slots(n, gamma)]
+  int *bucket = smem + list_slots(p.n, gamma) / 2;                     // [gamma]
   const int16_t *kcol = U.kstar + (size_t)g * p.ldk;
 
   // ---- bucket the selections of group g by perceptron (counting sort) -------
@@ -359,10 +421,12 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
   {
     // exclusive prefix sum of the bucket sizes: thread t owns buckets
     // [t ch, t ch + ch); a scan inside each wave, then across the waves
+    // (each row's slots padded to a multiple of 8, so that every row
+    // starts on a 16-byte boundary)
     const int ch = (gamma + kThreads - 1) / kThreads;
     const int b0 = min(gamma, tid * ch), b1 = min(gamma, b0 + ch);
     int own = 0;
-    for (int r = b0; r < b1; ++r) own += bucket[r];
+    for (int r = b0; r < b1; ++r) own += round8(bucket[r]);
     int inc = own;
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
@@ -376,7 +440,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     for (int r = b0; r < b1; ++r) {
       const int c = bucket[r];
       bucket[r] = run;
-      run += c;
+      run += round8(c);
     }
   }
   __syncthreads();
@@ -418,11 +482,14 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     }
   }
   __syncthreads();
-  // bucket[r] is now the end of row r's selectors; row r starts at bucket[r-1]
+  // bucket[r] is now the end of row r's selectors; row r starts at
+  // round8(bucket[r - 1])
 
   const int B = p.bound;
   const uint32_t t_hi = U.t_hi, t_lo = U.t_lo;
   const int groups_in = (U.k_in + 31) >> 5;   // 32-column groups of a row holding columns
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t *>(U.a32), 0, p.n * U.nw32 * 4, kRawRsrcWord3);
   int nreinf = 0;
 
   // work items: (row r, 2048-column chunk); lane l owns 32-column group
@@ -440,33 +507,30 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     const uint32_t validmask = nvalid == 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
     // the row's selector range is the same for every lane: scalars, so the
     // branches on S are scalar and its constants live in scalar registers
-    const int beg = __builtin_amdgcn_readfirstlane(r ? bucket[r - 1] : 0);
+    const int beg = __builtin_amdgcn_readfirstlane(r ? round8(bucket[r - 1]) : 0);
     const int S = __builtin_amdgcn_readfirstlane(bucket[r]) - beg;
 
-    // plane p of the lane's group: word p * h_ps + cwc of the row
-    uint32_t *urow = reinterpret_cast<uint32_t *>(U.H + (size_t)k * U.ld_h) + cwc;
-    uint32_t u[M];
-#pragma unroll
-    for (int q = 0; q < M; ++q) u[q] = urow[(size_t)q * U.h_ps];
-
-    // ---- coarse reinforcement draws: plane p of the 32 bytes is word p of
-    // Philox blocks 2 (k ceil(K/32) + group) and the one after (stream 3) ----
-    const uint32_t blk = 2u * ((uint32_t)k * (uint32_t)groups_in + (uint32_t)cwc);
     // per-item copies of the uniform constants: what is made from them is
     // made again in each item, in scalar registers, instead of held across
     // the loop
     const uint32_t key0 = opaque(p.key0), key1 = opaque(p.key1);
     const int Bi = (int)opaque((uint32_t)B);
     const uint32_t thi = opaque(t_hi);
-    const U32x4 v0 = philox4x32_10(blk, U.ctr1, p.step, kStreamCoarse, key0, key1);
-    const U32x4 v1 = philox4x32_10(blk + 1u, U.ctr1, p.step, kStreamCoarse, key0, key1);
 
     // ---- Clipped-Perceptron sum and clip ------------------------------------
+    // the counts first, then the H planes (loaded after the counting, so
+    // that they hold no registers during it)
+    const bool counted = S > 0 && !p.sequential;
+    uint32_t c[kPlanes];
+    if (counted) count_row(c, list, beg, S, rs, 4 * U.nw32, 4 * cwc);
+    // plane p of the lane's group: word p * h_ps + cwc of the row
+    uint32_t *urow = reinterpret_cast<uint32_t *>(U.H + (size_t)k * U.ld_h) + cwc;
+    uint32_t u[M];
+#pragma unroll
+    for (int q = 0; q < M; ++q) u[q] = urow[(size_t)q * U.h_ps];
     if (S > 0 && p.sequential) {
       cp_sequential<M>(u, list, beg, S, Bi, validmask, U.a32, U.nw32, cwc);
-    } else if (S > 0) {
-      uint32_t c[kPlanes];
-      count_row(c, list, beg, S, U.a32, U.nw32, cwc);
+    } else if (counted) {
       uint32_t un[M];
 #pragma unroll
       for (int q = 0; q < M; ++q) un[q] = u[q];
@@ -482,6 +546,13 @@ __global__ __launch_bounds__(kThreads) void update_kernel(UpdateBatch p) {
     }
     // sign(h) after the Clipped-Perceptron step; reinforcement keeps it
     const uint32_t pos = FULL ? u[M - 1] : at_least<M>(u, (Bi + 1) >> 1);
+
+    // ---- coarse reinforcement draws: plane p of the 32 bytes is word p of
+    // Philox blocks 2 (k ceil(K/32) + group) and the one after (stream 3)
+    // (drawn after the counting, so that they hold no registers during it) ----
+    const uint32_t blk = 2u * ((uint32_t)k * (uint32_t)groups_in + (uint32_t)cwc);
+    const U32x4 v0 = philox4x32_10(blk, U.ctr1, p.step, kStreamCoarse, key0, key1);
+    const U32x4 v1 = philox4x32_10(blk + 1u, U.ctr1, p.step, kStreamCoarse, key0, key1);
 
     // ---- which weights reinforce: u8 < T >> 24, or u8 == T >> 24 and the
     // fine 24 bits below T & 0xFFFFFF ---------------------------------------------
@@ -575,7 +646,7 @@ void launch_planes(bool full, dim3 grid, dim3 block, size_t lds, hipStream_t s, 
 }  // namespace
 
 size_t update_lds_bytes(int gamma, int n) {
-  return (size_t)gamma * sizeof(int) + (size_t)n * sizeof(uint16_t);
+  return (size_t)list_slots(n, gamma) * sizeof(uint16_t) + (size_t)gamma * sizeof(int);
 }
 
 hipError_t launch_update(UpdateBatch &b, hipStream_t s) {
