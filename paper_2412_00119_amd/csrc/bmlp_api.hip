@@ -125,24 +125,37 @@ inline hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s);
 
 bool use_mfma(const Plan &p) { return p.fwd_impl != BMLP_FWD_POPCOUNT; }
 
-// y_hat = a_l P_l^T of one layer by the forward kernel, for class counts
-// above what the classifier kernel takes: int32 rows [n][c] into y32, or
-// int16 rows [n][ldy16] into y16.
-FwdArgs cls_gemm_args(const Plan &p, int l, const uint64_t *a, const uint64_t *P, int n, int32_t *y32,
-                      int16_t *y16) {
-  const LayerPlan &lp = p.layer[l - 1];
+// y_hat = a_l P_l^T by the forward kernel, for class counts above what the
+// classifier kernel takes, up to kMaxFwdSlices layers per launch (once every
+// forward is done, so that the launch has the tiles of all of them): int32
+// rows [n][c] into y32, or int16 rows [n][ldy16] into y16, per layer.
+struct ClsGemm {
   FwdArgs g{};
-  g.A = a; g.lda = lp.words_out;
-  g.B = P; g.ldb = lp.words_out;
-  g.M = n; g.N = p.c; g.K = lp.k_out;
-  g.abits = nullptr; g.words_out = 0;
-  if (y32 != nullptr) {
-    g.mode = kFwdWriteZ32; g.z32 = y32; g.ldz = p.c;
-  } else {
-    g.mode = kFwdWriteZ; g.z = y16; g.ldz = p.ldy16;
+  ClsGemm(const Plan &p, int n, bool wide) {
+    g.M = n; g.N = p.c;
+    g.abits = nullptr; g.words_out = 0;
+    g.mode = wide ? kFwdWriteZ32 : kFwdWriteZ;
+    g.ldz = wide ? p.c : p.ldy16;
   }
-  return g;
-}
+  // layer l: a_l rows a, classifier rows P, output rows y32 or y16; true
+  // when the launch is full (flush it before the next add)
+  bool add(const Plan &p, int l, const uint64_t *a, const uint64_t *P, int32_t *y32, int16_t *y16) {
+    const LayerPlan &lp = p.layer[l - 1];
+    g.sl[g.nslices++] = FwdSlice{a, P, lp.words_out, lp.k_out, y16, y32};
+    return g.nslices == kMaxFwdSlices;
+  }
+  bool pending() const { return g.nslices > 0; }
+  hipError_t flush(hipStream_t s) {
+    if (g.nslices == 1) {   // the single-layer form
+      const FwdSlice q = g.sl[0];
+      g.A = q.A; g.B = q.B; g.lda = g.ldb = q.ld; g.K = q.K; g.z = q.z; g.z32 = q.z32;
+      g.nslices = 0;
+    }
+    const hipError_t e = launch_fwd_fp4(g, s);
+    g.nslices = 0;
+    return e;
+  }
+};
 
 // Forward of every layer for inference (y_hat out) or evaluation (counts:
 // layer l adds to correct[cstride * (l - 1)]; with flags, each pattern's
@@ -161,6 +174,7 @@ int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32
   if (use_mfma(p)) {
     const bool cls_gemm = p.c > kClsMaxClasses;
     int16_t *y16_ws = reinterpret_cast<int16_t *>(ctx->ws + p.off_yhat);
+    ClsGemm gemm(p, n, correct == nullptr);
     const uint64_t *a_prev = x;
     for (int l = 1; l <= p.L; ++l) {
       const LayerPlan &lp = p.layer[l - 1];
@@ -172,12 +186,14 @@ int forward_layers(bmlp_ctx *ctx, const uint64_t *x, int n, hipStream_t s, int32
       f.mode = kFwdPlain;
       BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s, launch_fwd_fp4(f, s));
       a_prev = f.abits;
-      if (cls_gemm) {   // y_hat of layer l while a_l is fresh in the caches
-        FwdArgs g = cls_gemm_args(p, l, a_prev, reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p), n,
-                                  correct ? nullptr : yhat_out + (size_t)(l - 1) * n * p.c,
-                                  y16_ws + (size_t)(l - 1) * p.max_batch * p.ldy16);
-        BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_fwd_fp4(g, s));
-      }
+    }
+    if (cls_gemm) {   // y_hat of every layer
+      for (int l = 1; l <= p.L; ++l)
+        if (gemm.add(p, l, a_of(l), reinterpret_cast<const uint64_t *>(ctx->state + p.layer[l - 1].off_p),
+                     correct ? nullptr : yhat_out + (size_t)(l - 1) * n * p.c,
+                     correct ? y16_ws + (size_t)(l - 1) * p.max_batch * p.ldy16 : nullptr))
+          BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, gemm.flush(s));
+      if (gemm.pending()) BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, gemm.flush(s));
     }
     if (cls_gemm && !correct) return BMLP_OK;   // y_hat is the output
     // every layer's local classifier (or, after the products above, its
@@ -467,10 +483,7 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
         ls.yhat = nullptr;
         BMLP_TIMED(ctx, BMLP_KERNEL_SELECT, s, launch_loss_select(ls, s));
       }
-      if (cls_gemm) {   // Algorithm 1's y_hat of layer l, while a_l is fresh in the caches
-        FwdArgs g = cls_gemm_args(p, l, a, P, n, nullptr, y16 + (size_t)(l - 1) * p.max_batch * p.ldy16);
-        BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, launch_fwd_fp4(g, s));
-      }
+
     } else {
       BMLP_TIMED(ctx, BMLP_KERNEL_FWD, s,
                  launch_fwd_popcount(a_prev, lp.words_in, lp.k_in, W, n, lp.k_out, z, p.ldz, a,
@@ -481,6 +494,17 @@ int bmlp_train_step(bmlp_ctx *ctx, const uint64_t *d_x, const int32_t *d_y, int3
       BMLP_TIMED(ctx, BMLP_KERNEL_SELECT, s, launch_loss_select(ls, s));
     }
     a_prev = a;
+  }
+  if (cls_gemm) {   // Algorithm 1's y_hat of every layer
+    ClsGemm gemm(p, n, false);
+    for (int l = 1; l <= p.L; ++l) {
+      const LayerPlan &lp = p.layer[l - 1];
+      if (gemm.add(p, l, reinterpret_cast<const uint64_t *>(ctx->ws + lp.off_a),
+                   reinterpret_cast<const uint64_t *>(ctx->state + lp.off_p), nullptr,
+                   y16 + (size_t)(l - 1) * p.max_batch * p.ldy16))
+        BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, gemm.flush(s));
+    }
+    if (gemm.pending()) BMLP_TIMED(ctx, BMLP_KERNEL_CLS, s, gemm.flush(s));
   }
   if (mfma) {
     // Algorithm 1's local output (or, after the products above, the error

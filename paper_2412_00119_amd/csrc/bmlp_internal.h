@@ -53,6 +53,16 @@ hipError_t launch_cls_popcount(const uint64_t *a, int words, int k, const uint64
 // a_l, B = P_l) when the classes are too many for the classifier kernel
 // (kFwdWriteZ or kFwdWriteZ32, words_out = 0: no sign bits).
 enum { kFwdFusedSelect = 0, kFwdWriteZ = 1, kFwdPlain = 2, kFwdWriteZ32 = 3 };
+// One layer of a launch: its operands (A and B rows share the stride ld),
+// K and z.  A launch of several slices (kFwdWriteZ or kFwdWriteZ32 only)
+// runs the nt_m x nt_n tiles of each in turn; M, N and ldz are common.
+struct FwdSlice {
+  const uint64_t *A, *B;
+  int ld, K;
+  int16_t *z;
+  int32_t *z32;
+};
+constexpr int kMaxFwdSlices = 8;
 struct FwdArgs {
   const uint64_t *A; int lda;       // a_{l-1} bit rows [M][lda words]
   const uint64_t *B; int ldb;       // W_l bit rows [N][ldb words]
@@ -66,6 +76,8 @@ struct FwdArgs {
   int32_t *z32;                     // kFwdWriteZ32: z int32 [M][ldz]
   float zlo, zhi;                   // kFwdFusedSelect: the selection clips z to [zlo, zhi]
   int32_t *zero; int nzero;         // if set: zeroed by the first work-group (step statistics)
+  int nslices;                      // > 1: sl[0 .. nslices) replace A, B, lda, ldb, K, z, z32
+  FwdSlice sl[kMaxFwdSlices];       // (for one slice the launcher fills sl[0] from those fields)
   int nt_m, nt_n, xcd_remap;        // set by the launcher (xcd_remap: 1 = slices of B, 2 = of A)
   int pw_max, ystride;              // set by the launcher: last word of a P row; label stride
 };

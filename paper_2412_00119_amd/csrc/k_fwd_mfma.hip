@@ -137,9 +137,13 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
 
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
+  // the slice (layer) of this work-group, then its tile
+  const int tiles = p.nt_m * p.nt_n;
+  const int sli = (int)blockIdx.x / tiles;
+  const FwdSlice S = p.sl[sli];   // a copy: kept in scalar registers
   int mt, nt;
   {
-    const int b = blockIdx.x;
+    const int b = (int)blockIdx.x - sli * tiles;
     if (p.xcd_remap == 1) {   // XCD x takes the x-th eighth of B's tiles
       const int x = b & 7, idx = b >> 3, per = p.nt_n >> 3;
       nt = x * per + idx / p.nt_m;
@@ -180,15 +184,15 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   // (only in the last step) is clamped to the row's last UNIT bytes.
   const uint8_t *srcA[kDma], *srcB[kDma];
   int offA[kDma];
-  const int rowbytes_a = 8 * p.lda, rowbytes_b = 8 * p.ldb;
+  const int rowbytes_a = 8 * S.ld, rowbytes_b = 8 * S.ld;
 #pragma unroll
   for (int h = 0; h < kDma; ++h) {
     const int pos = UNIT * lane;   // byte in the instruction's rows
     const int r = 32 * wave + kRowsPerDma * h + pos / KB;
     const int inrow = pos % KB;
     offA[h] = 16 * ((inrow / 16) ^ swz(r)) + inrow % 16;
-    srcA[h] = reinterpret_cast<const uint8_t *>(p.A + (size_t)min(m0 + r, p.M - 1) * p.lda);
-    srcB[h] = reinterpret_cast<const uint8_t *>(p.B + (size_t)min(n0 + r, p.N - 1) * p.ldb);
+    srcA[h] = reinterpret_cast<const uint8_t *>(S.A + (size_t)min(m0 + r, p.M - 1) * S.ld);
+    srcB[h] = reinterpret_cast<const uint8_t *>(S.B + (size_t)min(n0 + r, p.N - 1) * S.ld);
   }
   auto issue = [&](int ks, uint8_t *d) {
 #pragma unroll
@@ -261,7 +265,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     for (int c = 0; c < 2; ++c)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int nv = p.K - (512 * ks + 256 * c + 128 * ahalf + 32 * q);
+        const int nv = S.K - (512 * ks + 256 * c + 128 * ahalf + 32 * q);
         const uint32_t valid = nv >= 32 ? 0xFFFFFFFFu : nv <= 0 ? 0u : ((1u << nv) - 1u);
         uint4 ea[2], eb[2];
 #pragma unroll
@@ -287,8 +291,8 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   // compiler's wait-count tracking to merge over (a merge makes it wait for
   // every load before the next LDS read).  A partial last step is computed
   // after the loop.
-  const int nks = (p.K + 511) / 512;
-  const int nfull = p.K / 512;      // steps with no element past K
+  const int nks = (S.K + 511) / 512;
+  const int nfull = S.K / 512;      // steps with no element past K
   const int klast = nks - 1;        // nks >= 1
   if (wave == 0) {   // labels first: the oldest loads, covered by the prologue's wait
 #pragma unroll
@@ -476,9 +480,9 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
           if (m < p.M && col < p.N) {
             const size_t o = (size_t)m * p.ldz + col;
             if (wide)
-              p.z32[o] = (int)acc[i][j][e];
+              S.z32[o] = (int)acc[i][j][e];
             else
-              p.z[o] = (int16_t)(int)acc[i][j][e];
+              S.z[o] = (int16_t)(int)acc[i][j][e];
           }
         }
   }
@@ -489,39 +493,55 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
 
 hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  if (a.K < 1 || a.N < 1 || a.lda < (a.K + 63) / 64 || a.ldb < (a.K + 63) / 64) return hipErrorInvalidValue;
+  if (a.nslices <= 1) {   // one layer: its fields are slice 0
+    if (a.lda != a.ldb) return hipErrorInvalidValue;
+    a.nslices = 1;
+    a.sl[0] = FwdSlice{a.A, a.B, a.lda, a.K, a.z, a.z32};
+  } else if (a.nslices > kMaxFwdSlices || (a.mode != kFwdWriteZ && a.mode != kFwdWriteZ32)) {
+    return hipErrorInvalidValue;
+  }
+  const bool zout = a.mode == kFwdWriteZ || a.mode == kFwdWriteZ32;
+  if (a.N < 1 || (zout && a.ldz < a.N)) return hipErrorInvalidValue;
+  if (a.words_out > 0 && a.abits == nullptr) return hipErrorInvalidValue;
+  bool aligned = true;
+  double bytes_a = 0.0, bytes_b = 0.0;
+  for (int i = 0; i < a.nslices; ++i) {
+    const FwdSlice &q = a.sl[i];
+    if (q.A == nullptr || q.B == nullptr || q.K < 1 || q.ld < (q.K + 63) / 64) return hipErrorInvalidValue;
+    if ((a.mode == kFwdWriteZ && q.z == nullptr) || (a.mode == kFwdWriteZ32 && q.z32 == nullptr))
+      return hipErrorInvalidValue;
+    // rows start on 16-byte boundaries when the bases are 16-byte aligned
+    // and the stride is an even number of words
+    aligned = aligned && q.ld % 2 == 0 && (reinterpret_cast<uintptr_t>(q.A) & 15) == 0 &&
+              (reinterpret_cast<uintptr_t>(q.B) & 15) == 0;
+    bytes_a += (double)a.M * q.ld;
+    bytes_b += (double)a.N * q.ld;
+  }
   a.nt_m = (a.M + TM - 1) / TM;
   a.nt_n = (a.N + TN - 1) / TN;
   // each XCD keeps its slice of the larger operand in its own L2 (W_l in a
   // hidden layer; a_l when B is a narrow classifier matrix P_l)
-  if (a.nt_m % 8 == 0 && (double)a.M * a.lda > (double)a.N * a.ldb)
+  if (a.nt_m % 8 == 0 && bytes_a > bytes_b)
     a.xcd_remap = 2;
   else
     a.xcd_remap = (a.nt_n % 8 == 0) ? 1 : 0;
-  if (a.words_out > 0 && a.abits == nullptr) return hipErrorInvalidValue;
-  if ((a.mode == kFwdWriteZ && a.z == nullptr) || (a.mode == kFwdWriteZ32 && a.z32 == nullptr) ||
-      ((a.mode == kFwdWriteZ || a.mode == kFwdWriteZ32) && a.ldz < a.N))
-    return hipErrorInvalidValue;
   if (a.mode == kFwdFusedSelect) {
     if (a.y == nullptr || a.P == nullptr || a.c < 1) return hipErrorInvalidValue;
     a.pw_max = a.words_out - 1;
     a.ystride = 1;
-  } else {   // the label and rho loads read A instead (always valid)
-    a.y = reinterpret_cast<const int32_t *>(a.A);
+  } else {   // the label and rho loads read slice 0's A instead (always valid)
+    a.y = reinterpret_cast<const int32_t *>(a.sl[0].A);
     a.ystride = 0;
-    a.P = a.A;
+    a.P = a.sl[0].A;
     a.ldp = 0;
     a.c = 1;
     a.pw_max = 0;
   }
-  // rows start on 16-byte boundaries when the bases are 16-byte aligned and
-  // the strides are even numbers of words
-  const bool aligned = a.lda % 2 == 0 && a.ldb % 2 == 0 && (reinterpret_cast<uintptr_t>(a.A) & 15) == 0 &&
-                       (reinterpret_cast<uintptr_t>(a.B) & 15) == 0;
+  const dim3 grid(a.nslices * a.nt_m * a.nt_n);
   if (aligned)
-    hipLaunchKernelGGL(fwd_fp4_kernel<16>, dim3(a.nt_m * a.nt_n), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(fwd_fp4_kernel<16>, grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(fwd_fp4_kernel<4>, dim3(a.nt_m * a.nt_n), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(fwd_fp4_kernel<4>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

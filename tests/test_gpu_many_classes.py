@@ -1,7 +1,7 @@
 """Layers with more classes than the classifier kernel stages at once (above
 128): y_hat = a_l P_l^T then comes from the forward kernel with P_l in
-place of W_l (int16 rows inside a step or an evaluation, int32 rows as
-bmlp_forward's output), and the error signal of Eq. 1 and the robustness
+place of W_l, up to eight layers per launch (int16 rows inside a step or an
+evaluation, int32 rows as bmlp_forward's output), and the error signal of Eq. 1 and the robustness
 test from a separate kernel.  Bit-exact against the oracle: a_l, 01-loss,
 M_l, the selected perceptrons, the counts, H_l and W_l after every step;
 y_hat, correct counts and early-exit counts.  Narrow layers give y_hat few
@@ -30,6 +30,8 @@ CASES = [
     ((64, 8, 16), 200, 7, 8, 150, 2, 1.0),
     # a thousand classes, as in the 8192-wide stress network
     ((512, 640), 1000, 31, 64, 96, 2, 0.5),
+    # nine layers: the products of eight layers in one launch, then one more
+    ((100,) + (64,) * 9, 150, 7, 64, 70, 2, 0.5),
 ]
 
 
