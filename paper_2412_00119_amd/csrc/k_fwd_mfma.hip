@@ -118,8 +118,10 @@ __device__ __forceinline__ void select_step(uint32_t (&v)[32], int lc) {
 }
 
 // UNIT: bytes per lane of the direct-to-LDS loads, 16 when every operand
-// row starts on a 16-byte boundary, else 4
-template <int UNIT>
+// row starts on a 16-byte boundary, else 4.  SLICED: the launch covers
+// several layers (p.sl); a one-layer launch reads its fields directly, which
+// keeps the slice lookup out of its prologue.
+template <int UNIT, bool SLICED>
 __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   // one LDS array per ring slot (A tile, then B tile): every access below
   // names its array, so the compiler can tell a slot being read from the
@@ -138,12 +140,18 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
   // the slice (layer) of this work-group, then its tile
-  const int tiles = p.nt_m * p.nt_n;
-  const int sli = (int)blockIdx.x / tiles;
-  const FwdSlice S = p.sl[sli];   // a copy: kept in scalar registers
+  FwdSlice S;   // a copy: kept in scalar registers
+  int b = (int)blockIdx.x;
+  if constexpr (SLICED) {
+    const int tiles = p.nt_m * p.nt_n;
+    const int sli = b / tiles;
+    S = p.sl[sli];
+    b -= sli * tiles;
+  } else {
+    S = FwdSlice{p.A, p.B, p.lda, p.K, p.z, p.z32};
+  }
   int mt, nt;
   {
-    const int b = (int)blockIdx.x - sli * tiles;
     if (p.xcd_remap == 1) {   // XCD x takes the x-th eighth of B's tiles
       const int x = b & 7, idx = b >> 3, per = p.nt_n >> 3;
       nt = x * per + idx / p.nt_m;
@@ -493,7 +501,8 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
 
 hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  if (a.nslices <= 1) {   // one layer: its fields are slice 0
+  const bool sliced = a.nslices > 1;
+  if (!sliced) {   // one layer: its fields (checked as slice 0)
     if (a.lda != a.ldb) return hipErrorInvalidValue;
     a.nslices = 1;
     a.sl[0] = FwdSlice{a.A, a.B, a.lda, a.K, a.z, a.z32};
@@ -538,10 +547,14 @@ hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s) {
     a.pw_max = 0;
   }
   const dim3 grid(a.nslices * a.nt_m * a.nt_n);
-  if (aligned)
-    hipLaunchKernelGGL(fwd_fp4_kernel<16>, grid, dim3(256), 0, s, a);
+  if (aligned && sliced)
+    hipLaunchKernelGGL((fwd_fp4_kernel<16, true>), grid, dim3(256), 0, s, a);
+  else if (aligned)
+    hipLaunchKernelGGL((fwd_fp4_kernel<16, false>), grid, dim3(256), 0, s, a);
+  else if (sliced)
+    hipLaunchKernelGGL((fwd_fp4_kernel<4, true>), grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(fwd_fp4_kernel<4>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((fwd_fp4_kernel<4, false>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
