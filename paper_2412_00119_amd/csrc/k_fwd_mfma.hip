@@ -3,13 +3,18 @@
 // the epilogue.
 //
 // The operands are the bit rows the rest of the step keeps (bit 1 = +1):
-// a_{l-1} (or the input) and W_l.  Each 32-bit word is expanded in registers
-// to an OCP e2m1 (fp4) MFMA operand, +1 -> 0x2 and -1 -> 0xA, in the K order
-// of fp4x32_permuted; both operands use that order, so every dot product is
-// unchanged.  v_mfma_scale_f32_32x32x64_f8f6f4 multiplies ±1 by ±1 exactly
-// and accumulates in fp32, exact for |z| < 2^24 (on gfx950 the 32x32x64
-// shape runs fp4 at twice the rate of 16x16x128).  The expansion is a few
-// bit operations per MFMA, issued between the MFMAs of the same wave.
+// a_{l-1} (or the input) and W_l, made into OCP e2m1 (fp4) MFMA operands in
+// registers by K class (element k is in class k mod 4; see class_bits): the
+// sign class as ±1 (0x2 / 0xA), the other three as the bit alone, 0 or a
+// power of two, which takes one bit operation per operand word instead of a
+// shift and a merge.  The accumulators then hold z_3 + 4 C (C counting the
+// elements of classes 0..2 where both bits are 1), and the epilogue adds
+// n_low - 2 (P_a + P_w) from per-row popcounts with one fp32 MFMA per
+// accumulator, which gives z exactly.  v_mfma_scale_f32_32x32x64_f8f6f4
+// multiplies these values exactly and accumulates in fp32, exact below 2^24
+// (on gfx950 the 32x32x64 shape runs fp4 at twice the rate of
+// 16x16x128).  A wave issues its MFMAs and bit operations one after the
+// other, so fewer VALU instructions per MFMA is a shorter K loop.
 //
 // A work-group computes a 128 x 128 tile of z (patterns x perceptrons) with
 // four waves of 64 x 64.  K is walked in steps of 512 elements (64 bytes of
@@ -93,16 +98,45 @@ __device__ __forceinline__ int swz(int r) { return (r >> 2) & 3; }
 // lane l: A row / B column (l & 31), half (l >> 5) of the 64-element K
 // block; result element i of lane l is row 8*(i>>2) + 4*(l>>5) + (i&3),
 // column (l & 31)
-__device__ __forceinline__ v16f mfma_fp4(const uint4 &a, const uint4 &b, v16f c) {
-  const v8i av = {(int)a.x, (int)a.y, (int)a.z, (int)a.w, 0, 0, 0, 0};
-  const v8i bv = {(int)b.x, (int)b.y, (int)b.z, (int)b.w, 0, 0, 0, 0};
-  // operand formats 4 = e2m1 for A and B, unit (E8M0 127) block scales
-  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, c, 4, 4, 0, 127, 0, 127);
+// K classes.  Element k of a bit row is in class k mod 4: bit s = k mod 4
+// of nibble t of its 32-bit word (the word holds elements 4t + s).  The
+// MFMA of class s over a 256-element chunk takes, from each of the lane's
+// four words, the bits of class s in place (nibble t of dword d = bit 4t + s
+// of word d); A and B use the same map, so every product pairs the same k.
+//   * class 3 is the e2m1 sign bit: bit 1 -> 0x2 (+1), bit 0 -> 0xA (-1),
+//     one v_bitop3; its MFMA adds z_3 = sum over class-3 k of a_k w_k;
+//   * classes 0..2 keep the bit alone (one AND): 0 or 2^(s-1) (0.5, 1, 2);
+//     with block scales 2^(2-s) on both operands the MFMA adds 4 for every
+//     k where both bits are 1.
+// So acc = z_3 + 4 C, C = #{k in classes 0..2: a-bit = w-bit = 1}, and
+// z = acc + n_low - 2 (P_a + P_w), where P_a and P_w are the rows'
+// popcounts over classes 0..2 and n_low = K - floor(K / 4) the class 0..2
+// elements of a row.  Every value is an integer below 2^24: exact in fp32.
+__device__ __forceinline__ uint32_t class_bits(uint32_t w, int s) {
+  return s == 3 ? fp4_sign_nibbles(w) : (w & (0x11111111u << s));
+}
+__device__ __forceinline__ uint4 class_operand(const uint4 &w, int s) {
+  return make_uint4(class_bits(w.x, s), class_bits(w.y, s), class_bits(w.z, s), class_bits(w.w, s));
+}
+// the elements whose bit in valid is 0 become fp4 zeros (past K)
+__device__ __forceinline__ uint32_t class_bits_masked(uint32_t w, uint32_t valid, int s) {
+  if (s == 3) return fp4_sign_nibbles(w) & (((valid & 0x88888888u) >> 3) * 0xFu);
+  return w & valid & (0x11111111u << s);
 }
 
-__device__ __forceinline__ uint32_t dword(const uint4 &u, int q) {
-  return q == 0 ? u.x : q == 1 ? u.y : q == 2 ? u.z : u.w;
+// lane l: A row / B column (l & 31), half (l >> 5) of the 64-element K
+// block; result element i of lane l is row 8*(i>>2) + 4*(l>>5) + (i&3),
+// column (l & 31)
+__device__ __forceinline__ v16f mfma_class(const uint4 &a, const uint4 &b, v16f c, int s) {
+  const v8i av = {(int)a.x, (int)a.y, (int)a.z, (int)a.w, 0, 0, 0, 0};
+  const v8i bv = {(int)b.x, (int)b.y, (int)b.z, (int)b.w, 0, 0, 0, 0};
+  // operand formats 4 = e2m1 for A and B; E8M0 block scales 2^(2-s) for
+  // classes 0..2 (129, 128, 127), 1 for the sign class
+  const int sc = s == 0 ? 129 : s == 1 ? 128 : 127;
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, c, 4, 4, 0, sc, 0, sc);
 }
+
+constexpr uint32_t kLowClasses = 0x77777777u;   // the bits of classes 0..2
 
 // one reduce-scatter step at lane distance D, the partner given by DPP
 // control CTRL: rows k + D move into slot k on lanes with bit D set
@@ -131,6 +165,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   __shared__ __align__(16) uint8_t s0[kSlot], s1[kSlot], s2[kSlot], s3[kSlot];
   __shared__ uint64_t sP[2][TM];       // rho^{y^mu} bits of the tile's 128 columns, per group
   __shared__ int32_t sY[TM];           // labels of the tile's rows
+  __shared__ uint32_t sPc[TM + TN];    // popcounts P_a (tile rows), then P_w (tile columns)
   static_assert(kStages == 4, "one named array per slot");
   constexpr int kRowsPerDma = 64 * UNIT / KB;     // rows per load instruction: 16 or 4
   constexpr int kDma = 32 / kRowsPerDma;          // instructions per operand per wave and step
@@ -244,11 +279,11 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   struct Exp {
     uint4 a[2], b[2];
   };
-  auto expand = [&](const Ops &o, int c, int q, Exp &e) {
+  auto expand = [&](const Ops &o, int c, int cls, Exp &e) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) e.a[i] = fp4x32_permuted(dword(o.a[c][i], q));
+    for (int i = 0; i < 2; ++i) e.a[i] = class_operand(o.a[c][i], cls);
 #pragma unroll
-    for (int j = 0; j < 2; ++j) e.b[j] = fp4x32_permuted(dword(o.b[c][j], q));
+    for (int j = 0; j < 2; ++j) e.b[j] = class_operand(o.b[c][j], cls);
   };
   auto compute_pipe = [&](const Ops &o, const Exp &e0, const Ops &onext, Exp &e0next) {
     Exp e = e0;
@@ -262,30 +297,73 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mfma_fp4(e.a[i], e.b[j], acc[i][j]);
+        for (int j = 0; j < 2; ++j) acc[i][j] = mfma_class(e.a[i], e.b[j], acc[i][j], blk & 3);
       if (blk < 7) e = en;
     }
   };
+  // Row popcounts of classes 0..2 (P_a for the A rows, P_w for the B rows),
+  // from the operand words the lanes already hold: wave (wm, wn) counts A
+  // fragment wn and B fragment wm, so every tile row and column is counted
+  // once, lane l over half (l >> 5) of the row (a wave-uniform branch picks
+  // the fragments: a select would cost a VALU instruction per word).  m[q]:
+  // the bits of word q of a chunk that count.
+  uint32_t pca = 0u, pcb = 0u;
+  auto popc4 = [](const uint4 &w, const uint32_t (&m)[4]) {
+    return __popc(w.x & m[0]) + __popc(w.y & m[1]) + __popc(w.z & m[2]) + __popc(w.w & m[3]);
+  };
+  auto popc_ops = [&](const Ops &o, const uint32_t (&m0)[4], const uint32_t (&m1)[4]) {
+    if (wn == 0)
+      pca += popc4(o.a[0][0], m0) + popc4(o.a[1][0], m1);
+    else
+      pca += popc4(o.a[0][1], m0) + popc4(o.a[1][1], m1);
+    if (wm == 0)
+      pcb += popc4(o.b[0][0], m0) + popc4(o.b[1][0], m1);
+    else
+      pcb += popc4(o.b[0][1], m0) + popc4(o.b[1][1], m1);
+  };
+  const uint32_t kFull[4] = {kLowClasses, kLowClasses, kLowClasses, kLowClasses};
   // the last step when K is not a multiple of 512: elements past K become
   // fp4 zeros in the W_l operand
   auto compute_tail = [&](const Ops &o, int ks) {
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < 2; ++c) {
+      uint32_t valid[4];   // valid bits of the lane's four words of chunk c
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int nv = S.K - (512 * ks + 256 * c + 128 * ahalf + 32 * q);
-        const uint32_t valid = nv >= 32 ? 0xFFFFFFFFu : nv <= 0 ? 0u : ((1u << nv) - 1u);
+        valid[q] = nv >= 32 ? 0xFFFFFFFFu : nv <= 0 ? 0u : ((1u << nv) - 1u);
+      }
+      uint32_t mv[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) mv[q] = valid[q] & kLowClasses;
+      if (wn == 0)
+        pca += popc4(o.a[c][0], mv);
+      else
+        pca += popc4(o.a[c][1], mv);
+      if (wm == 0)
+        pcb += popc4(o.b[c][0], mv);
+      else
+        pcb += popc4(o.b[c][1], mv);
+#pragma unroll
+      for (int cls = 0; cls < 4; ++cls) {
         uint4 ea[2], eb[2];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) ea[i] = fp4x32_permuted(dword(o.a[c][i], q));
+        for (int i = 0; i < 2; ++i) ea[i] = class_operand(o.a[c][i], cls);
 #pragma unroll
-        for (int j = 0; j < 2; ++j) eb[j] = fp4x32_permuted_masked(dword(o.b[c][j], q), valid);
+        for (int j = 0; j < 2; ++j) {
+          const uint4 w = o.b[c][j];
+          eb[j] = make_uint4(class_bits_masked(w.x, valid[0], cls), class_bits_masked(w.y, valid[1], cls),
+                             class_bits_masked(w.z, valid[2], cls), class_bits_masked(w.w, valid[3], cls));
+        }
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
-          for (int j = 0; j < 2; ++j) acc[i][j] = mfma_fp4(ea[i], eb[j], acc[i][j]);
+          for (int j = 0; j < 2; ++j) acc[i][j] = mfma_class(ea[i], eb[j], acc[i][j], cls);
       }
+    }
   };
+
+
 
   // Pipeline of step ks: the loads of step ks+3 are issued into the slot of
   // step ks-1, the MFMAs of step ks run on operands read during step ks-1,
@@ -332,8 +410,8 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     __builtin_amdgcn_sched_barrier(0);
     read(nxt, rs);   // past the last step this reads a slot nobody uses
     compute_pipe(cur, ecur, nxt, enxt);
-    // The order of the step's instructions: each MFMA followed by a seventh
-    // of the next K block's expansion, so that the VALU work runs while the
+    // The order of the step's instructions: each MFMA followed by a quarter
+    // of the next K block's operands, so that the VALU work runs while the
     // matrix core works on the MFMA; one LDS read after each of the first
     // eight MFMAs (issued before them, the reads would share the wait-count
     // of the operands being consumed).
@@ -341,9 +419,10 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     for (int i = 0; i < 32; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
       if (i < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
-      __builtin_amdgcn_sched_group_barrier(0x002, 7, 0);   // VALU
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);   // VALU
     }
     __builtin_amdgcn_sched_barrier(0);
+    popc_ops(cur, kFull, kFull);
   };
   // step ks reads slot (ks+1) % 4 and refills slot (ks+3) % 4
   int ks = 0;
@@ -369,9 +448,44 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   if (nfull < nks) compute_tail(r0, nfull);
 
   // ---- epilogue ---------------------------------------------------------------
+  // The row popcounts and the rho words reach every wave through LDS.  A
+  // plain barrier after the LDS writes: a __syncthreads fence would also
+  // wait for the repeated loads of the last steps, which land during the
+  // epilogue instead (and are waited for before the wave ends).
+  {
+    // the two halves of each row (lanes l and l + 32)
+    const uint32_t ta = pca + (uint32_t)__shfl_xor((int)pca, 32, 64);
+    const uint32_t tb = pcb + (uint32_t)__shfl_xor((int)pcb, 32, 64);
+    if (lane < 32) {
+      sPc[wm * 64 + wn * 32 + lane] = ta;
+      sPc[TM + wn * 64 + wm * 32 + lane] = tb;
+    }
+  }
+  sP[pw][pr] = pvalid ? prow : 0ull;
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0) only
+  __builtin_amdgcn_s_barrier();
+
   // lane holds z for column n0 + wn*64 + j*32 + (lane & 31) and rows
   // m0 + wm*64 + i*32 + 8*(e >> 2) + 4*(lane >> 5) + (e & 3) in acc[i][j][e]
   const int lh = lane >> 5, lc = lane & 31;
+  // z = acc + (n_low - 2 P_a[row]) + (-2 P_w[column]): a rank-2 term, added
+  // exactly by one fp32 MFMA with K = 2 per accumulator (lane l holds A row
+  // (l & 31) at k = l >> 5 and B column (l & 31) at k = l >> 5):
+  // A = (n_low - 2 P_a, 1), B = (1, -2 P_w)
+  {
+    const float nlow = (float)(S.K - S.K / 4);
+    float fa[2], fb[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      fa[i] = lh == 0 ? nlow - 2.f * (float)sPc[wm * 64 + i * 32 + lc] : 1.f;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      fb[j] = lh == 0 ? 1.f : -2.f * (float)sPc[TM + wn * 64 + j * 32 + lc];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i], fb[j], acc[i][j], 0, 0, 0);
+  }
   // a_l = sign(z): the ballot of (i, j, e) holds the signs of 32 columns
   // (half j of the wave's 64) of two rows (lanes 0-31 and 32-63).  Ballot
   // k = 16 (2i + j) + e is moved to lane k, which then writes both rows' 32
@@ -403,15 +517,6 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
       if (m < p.M && cw < 2 * p.words_out) ab32[(size_t)m * 2 * p.words_out + cw] = h ? bhi : blo;
     }
   }
-
-  // The rho words reach every wave through LDS.  A plain barrier after the
-  // LDS writes: a
-  // __syncthreads fence would also wait for the repeated loads of the last
-  // steps, which land during the epilogue instead (and are waited for
-  // before the wave ends).
-  sP[pw][pr] = pvalid ? prow : 0ull;
-  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0) only
-  __builtin_amdgcn_s_barrier();
 
   if (p.mode == kFwdFusedSelect) {
     const int gcol0 = n0 + wn * 64;   // the wave's 64 columns are one group
