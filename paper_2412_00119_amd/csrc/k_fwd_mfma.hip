@@ -525,11 +525,11 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
       // Key of each of the lane's 32 rows q = 16*i + e over its 2 columns,
       // formed on the bits of the exact fp32 z: with s = -z where the
       // classifier weight is +1 and s = z where it is -1, perceptron k is
-      // wrong iff s >= 1, and t = s - 0.5 is then positive with |z| - 0.5 in
-      // its magnitude (at most 16 significant bits, as |z| <= K_{l-1} <=
-      // 32767, so the low 8 bits are zero and take the column).  Unsigned
-      // order of bits(t) | k is (|z|, k) over the wrong perceptrons, and
-      // every right one (t < 0, sign bit set) comes after them.
+      // wrong iff s >= 1.  s is an integer with |s| <= K_{l-1} <= 32767, so
+      // the low 8 bits of bits(s) are zero, and key = bits(s) - bits(1.0f) +
+      // k (mod 2^32) is below 2^27 exactly for the wrong perceptrons, in
+      // the order (|z|, k); every right one (s = +0 wraps, s = -0 and s < 0
+      // have the sign bit) gets a key of at least 2^30.
       const uint32_t sh = 31u - (uint32_t)lc;
       uint32_t v[32];
       // z as the selection sees it: clipped only where [zlo, zhi] is
@@ -548,7 +548,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
               const uint32_t r = (uint32_t)(rho >> (32 * j)) << sh;   // bit 31: rho of column j*32 + lc
               const float zc = kClip ? fminf(fmaxf(acc[i][j][e], p.zlo), p.zhi) : acc[i][j][e];
               const float sz = __uint_as_float(__float_as_uint(zc) ^ (r & 0x80000000u));
-              key[j] = __float_as_uint(sz - 0.5f) | (uint32_t)(j * 32 + lc);
+              key[j] = __float_as_uint(sz) + ((uint32_t)(j * 32 + lc) - 0x3F800000u);
             }
             v[i * 16 + e] = min(key[0], key[1]);
           }
@@ -578,7 +578,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
       const int i = lc >> 4, e = lc & 15;
       const int rl = wm * 64 + i * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
       const int m = m0 + rl;
-      if (m < p.M) p.kstar[(size_t)g * p.ldk + m] = (v[0] >> 31) ? (int16_t)-1 : (int16_t)(v[0] & 0x3Fu);
+      if (m < p.M) p.kstar[(size_t)g * p.ldk + m] = (v[0] >= (1u << 27)) ? (int16_t)-1 : (int16_t)(v[0] & 0x3Fu);
     }
   } else if (p.mode == kFwdWriteZ || p.mode == kFwdWriteZ32) {
     const bool wide = p.mode == kFwdWriteZ32;
