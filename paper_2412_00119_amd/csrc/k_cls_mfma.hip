@@ -4,35 +4,48 @@
 // independent once every forward is done, so one launch covers them all.
 //
 // A work-group owns 16 patterns of one layer and all its classes, up to
-// kClsMaxClasses of them: CB blocks of 16 classes (CB is a template
-// parameter sized to the class count).  a_l and P_l are read as bit rows:
-// chunks of 4096 columns of the 16 pattern rows and the class rows are
-// staged in LDS with coalesced loads (a load that touched 16 rows at once
-// cost 16 cache-line requests, which bound the kernel), rows padded so that
-// operand reads hit 64 banks.  A lane takes one 32-bit word (32 elements of
-// a 128-element K step) of its row and expands it in registers to an fp4
-// operand; the expansion permutes K inside the word, identically for a_l
-// and P_l, which leaves every dot product unchanged.  Elements past K_l
-// become fp4 zeros in the P operand.  Rows past n or c repeat the last row:
-// they only feed y_hat entries that are never read.
+// kClsMaxClasses of them: CB blocks of 16 classes (CB, a template parameter,
+// is the exact block count).  Its four waves split K: wave w takes the
+// super-blocks w, w + 4, ... of 512 elements, over every class block, so
+// that a_l's rows are read once per work-group and each wave's a_l operand
+// serves all CB blocks.  a_l and P_l are read as bit rows straight into
+// registers, lane (r, q) holding the 16 bytes 16q .. 16q + 15 of the
+// super-block's 64 bytes of row r (elements 128q .. 128q + 127: four 32-bit
+// words); the loads of CH super-blocks are all issued before their MFMAs
+// (for a 4096-wide layer with more than 64 classes, every load of the wave).
 //
-// The waves form KG groups along K times kWaves / KG groups along the
-// classes: a wave runs one v_mfma_scale_f32_16x16x128_f8f6f4 per K step for
-// each of its PB class blocks, over the chunk's K steps kg, kg + KG, ....
-// The partial sums are exact integers: each K group stores its int32
-// partials in LDS (over the staged chunk) and every thread then adds the KG
-// partials of its own y_hat entries, in a fixed order.
+// Operands by K class (element k in class k mod 4, bit 4t + s of a word in
+// class s): the MFMA of class s takes, from each of the lane's four words,
+// the bits of class s in place (nibble t of dword d = bit 4t + s of word d;
+// both operands use the same map, so every product pairs the same k).
+//   * a_l as ±1 in every class (the e2m1 sign bit made from the element's
+//     bit: a shift to bit 3 and one bit operation);
+//   * P_l as ±1 in class 3 and, in classes 0..2, as the bit alone (0 or
+//     2^(s-1)) with block scale 2^(2-s), so that a product is 2 (2a - 1) p
+//     for bits a, p.
+// The accumulator then holds y' = y_hat + 2 P_a - n_low, with P_a the
+// pattern row's popcount over classes 0..2 and n_low = K - floor(K / 4)
+// its class 0..2 elements (2 (2a - 1) p - (2a - 1)(2p - 1) = 2a - 1).  The
+// offset is the same for every class of a pattern, so the argmax and the
+// margin tau are those of y_hat; y_hat itself (kClsYhatOnly) subtracts it,
+// with P_a counted from the same words.  Every value is an integer below
+// 2^24, exact in fp32.  Elements past K_l become fp4 zeros in the P
+// operand; rows past n or c repeat the last row and only feed entries that
+// are never read.
 //
-// Then sixteen lanes take each pattern: first argmax (lowest class on
+// The accumulators go to LDS (the four K groups' partials are added when
+// read), then sixteen lanes take each pattern: first argmax (lowest class on
 // ties), the two largest values (tau = top1 - top2, 0 on a tie), err =
 // (pred != y) and upd = err or tau < ceil(r K_l).
 //
-// With more classes, staging every class row for each 16 patterns would
+// With more classes, loading every class row for each 16 patterns would
 // read P_l n / 16 times over; y_hat then comes from the forward kernel (a
 // tiled contraction with P_l in place of W_l, which reads each operand tile
 // once per output tile), and cls_argmax_kernel below takes the same error
 // signal from the stored y_hat, one wave per pattern.
 #include <limits.h>
+
+#include <type_traits>
 
 #include "bmlp_internal.h"
 #include "fp4.h"
@@ -43,12 +56,52 @@ namespace {
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = 8;
+constexpr int kWaves = 4;
 
-__device__ __forceinline__ v4f mfma_fp4(const uint4 &a, const uint4 &b, v4f c) {
+// the class-s operand of a pattern's words: ±1 from bit 4t + s of each word
+__device__ __forceinline__ uint32_t pm1_class(uint32_t w, int s) {
+  return fp4_sign_nibbles(s == 3 ? w : w << (3 - s));
+}
+__device__ __forceinline__ uint4 pm1_operand(const uint4 &w, int s) {
+  return make_uint4(pm1_class(w.x, s), pm1_class(w.y, s), pm1_class(w.z, s), pm1_class(w.w, s));
+}
+__device__ __forceinline__ uint4 bit_operand(const uint4 &w, int s) {
+  return make_uint4(class_bits(w.x, s), class_bits(w.y, s), class_bits(w.z, s), class_bits(w.w, s));
+}
+__device__ __forceinline__ uint4 bit_operand_masked(const uint4 &w, const uint32_t (&v)[4], int s) {
+  return make_uint4(class_bits_masked(w.x, v[0], s), class_bits_masked(w.y, v[1], s),
+                    class_bits_masked(w.z, v[2], s), class_bits_masked(w.w, v[3], s));
+}
+
+// lane l: A row / B column (l & 15), elements 32 (l >> 4) .. +31 of the
+// 128-element K block; result element e of lane l is row 4 (l >> 4) + e,
+// column (l & 15).  Operand formats 4 = e2m1; E8M0 block scales: 1 for the
+// patterns, class_scale(s) for the classifier rows.
+__device__ __forceinline__ v4f mfma_fp4(const uint4 &a, const uint4 &b, v4f c, int s) {
   const v8i av = {(int)a.x, (int)a.y, (int)a.z, (int)a.w, 0, 0, 0, 0};
   const v8i bv = {(int)b.x, (int)b.y, (int)b.z, (int)b.w, 0, 0, 0, 0};
-  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(av, bv, c, 4, 4, 0, 127, 0, 127);
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(av, bv, c, 4, 4, 0, 127, 0, class_scale(s));
+}
+
+// 16 bytes at byte o of a bit row of rowbytes bytes (a multiple of 8), zero
+// past its end; rows start on 16-byte boundaries when ALIGNED, else on
+// 8-byte ones
+template <bool ALIGNED>
+__device__ __forceinline__ uint4 load16(const uint8_t *row, int o) {
+  if constexpr (ALIGNED) {
+    return *reinterpret_cast<const uint4 *>(row + o);
+  } else {
+    const uint2 lo = *reinterpret_cast<const uint2 *>(row + o);
+    const uint2 hi = *reinterpret_cast<const uint2 *>(row + o + 8);
+    return make_uint4(lo.x, lo.y, hi.x, hi.y);
+  }
+}
+template <bool ALIGNED>
+__device__ __forceinline__ uint4 load16_tail(const uint8_t *row, int o, int rowbytes) {
+  if (o + 16 <= rowbytes) return load16<ALIGNED>(row, o);
+  uint2 lo = make_uint2(0u, 0u);
+  if (o + 8 <= rowbytes) lo = *reinterpret_cast<const uint2 *>(row + o);
+  return make_uint4(lo.x, lo.y, 0u, 0u);
 }
 
 struct Top2 {
@@ -80,187 +133,192 @@ __device__ __forceinline__ Top2 dpp_top2(const Top2 &t) {
 
 template <int CB>
 struct ClsShape {
-  static constexpr int PB = CB < 4 ? CB : 4;     // class blocks per wave
-  static constexpr int CG = CB / PB;             // wave groups along the classes
-  static constexpr int KG = kWaves / CG;         // wave groups along K
+  static constexpr int KG = kWaves;              // wave groups along K (each wave takes every class block)
+  static constexpr int CH = CB > 4 ? 2 : 4;      // super-blocks per load round
+  static constexpr int LD = CB * 16 + 4;         // LDS row stride of the partials
 };
 
-// K is staged through LDS in chunks of kChunk 32-bit words (4096 elements)
-// per row; rows are padded to kStride words (kStride = 4 mod 64), so the
-// lanes of an operand read (16 rows x 4 consecutive words) hit 64 banks.
-constexpr int kChunk = 128, kStride = kChunk + 4;
-
-template <int CB>
+// ALIGNED: every row starts on a 16-byte boundary.  YHAT: y_hat is the
+// output (kClsYhatOnly); otherwise the error signal (kClsTrain, kClsEval).
+template <int CB, bool ALIGNED, bool YHAT>
 __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
-  constexpr int PB = ClsShape<CB>::PB, KG = ClsShape<CB>::KG;
-  constexpr int kRows = 16 + CB * 16;                      // staged rows: 16 patterns, CB*16 classes
-  constexpr int kStage = kRows * kStride;                  // words
-  constexpr int kRed = KG * 16 * CB * 16;                  // words of the partials
-  __shared__ __align__(16) uint32_t lds[kStage > kRed ? kStage : kRed];
-  uint32_t *const sA = lds, *const sP = lds + 16 * kStride;
-  int (*red)[16][CB * 16] = reinterpret_cast<int (*)[16][CB * 16]>(lds);   // per K group; red[0] ends with y_hat
+  constexpr int KG = ClsShape<CB>::KG, CH = ClsShape<CB>::CH, LD = ClsShape<CB>::LD;
+  __shared__ int red[KG][16][LD];        // y' partials of the K groups
+  __shared__ int spa[KG][16];            // YHAT: P_a partials of the K groups
   __shared__ int cnt[3];                 // block totals of err, upd, correct
 
-  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
-  const int kg = wave % KG, cg = wave / KG;
+  const int tid = threadIdx.x, kg = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int bpl = (p.n + 15) / 16;               // work-groups per layer
   const ClsLayer &Lr = p.L[blockIdx.x / bpl];
   const int m0 = (blockIdx.x % bpl) * 16;
-  const int lr = lane & 15, q = lane >> 4;   // row / class, and which 32 of a K step's 128
-  const int nb = (p.c + 15) / 16;                 // class blocks (<= CB)
-  const uint32_t *A32 = reinterpret_cast<const uint32_t *>(Lr.A);
-  const uint32_t *P32 = reinterpret_cast<const uint32_t *>(Lr.P);
-  const int w32 = 2 * Lr.words;                  // 32-bit words per row
+  const int lr = lane & 15, q = lane >> 4;       // row / class, and which 16 bytes of a super-block
+  const int K = Lr.K;
   if (tid < 3) cnt[tid] = 0;
+  const int mu = m0 + 4 * kg + q;                // the argmax: waves 0..3 take 4 patterns each
+  int label = 0;
+  // Every argument the end of the kernel needs, read now: left to itself the
+  // compiler loads them where they are used, one dependent scalar load after
+  // another, each a miss that the argmax then waits for.
+  const int mode = p.mode, thr = Lr.thr;
+  uint8_t *const err_out = Lr.err, *const upd_out = Lr.upd, *const flag_out = Lr.flag;
+  int32_t *const stats_out = Lr.stats, *const correct_out = Lr.correct, *const yhat_out = Lr.yhat;
+  asm volatile("" ::"s"(mode), "s"(thr), "s"(err_out), "s"(upd_out), "s"(flag_out), "s"(stats_out),
+               "s"(correct_out), "s"(yhat_out));
 
-  v4f acc[PB];
+  // the lane's 16 bytes of each super-block start at row + 64 sb
+  const uint8_t *rowA = reinterpret_cast<const uint8_t *>(Lr.A + (size_t)min(m0 + lr, p.n - 1) * Lr.words) + 16 * q;
+  const uint8_t *rowP[CB];
 #pragma unroll
-  for (int j = 0; j < PB; ++j) acc[j] = (v4f){0.f, 0.f, 0.f, 0.f};
-  for (int kw0 = 0; kw0 < w32; kw0 += kChunk) {
-    // stage words kw0 .. kw0 + kChunk of the 16 pattern rows and the class
-    // rows, 16 bytes per thread, coalesced along rows; rows past n or c
-    // repeat the last row, words past the row are 0
-    __syncthreads();   // the previous chunk is no longer read
-    constexpr int kLoads = kRows * (kChunk / 4);                      // 16-byte pieces
-    constexpr int kPer = (kLoads + 64 * kWaves - 1) / (64 * kWaves);    // per thread
-    uint4 v[kPer];
+  for (int j = 0; j < CB; ++j)
+    rowP[j] = reinterpret_cast<const uint8_t *>(Lr.P + (size_t)min(j * 16 + lr, p.c - 1) * Lr.words) + 16 * q;
+  const int rowlim = 8 * Lr.words - 16 * q;      // bytes of the row from the lane's first byte
+
+  v4f acc[CB];
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) {   // all loads in flight before any store
-      const int t = min(tid + i * 64 * kWaves, kLoads - 1);
-      const int row = t / (kChunk / 4), w = kw0 + (t % (kChunk / 4)) * 4;
-      const uint32_t *src = row < 16 ? A32 + (size_t)min(m0 + row, p.n - 1) * w32
-                                     : P32 + (size_t)min(row - 16, p.c - 1) * w32;
-      // rows are whole u64 words (8-byte aligned), and w32 is even
-      uint2 lo = make_uint2(0u, 0u), hi = make_uint2(0u, 0u);
-      if (w < w32) lo = *reinterpret_cast<const uint2 *>(src + w);
-      if (w + 2 < w32) hi = *reinterpret_cast<const uint2 *>(src + w + 2);
-      v[i] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  for (int j = 0; j < CB; ++j) acc[j] = (v4f){0.f, 0.f, 0.f, 0.f};
+  int pa = 0;   // YHAT: P_a over the lane's words
+  auto popc_low = [](const uint4 &w) {
+    return __popc(w.x & kLowClasses) + __popc(w.y & kLowClasses) + __popc(w.z & kLowClasses) +
+           __popc(w.w & kLowClasses);
+  };
+  const int nfull = K / 512, nsb = (K + 511) / 512;
+  const int nf = nfull > kg ? (nfull - kg + KG - 1) / KG : 0;   // the wave's whole super-blocks: kg + KG i
+  // super-blocks i .. i + N - 1 of the wave: every load first, then the
+  // MFMAs, each waiting only for its own operands
+  auto run = [&](auto n_tag, int i) {
+    constexpr int N = decltype(n_tag)::value;
+    uint4 wa[N], wb[N][CB];
+#pragma unroll
+    for (int u = 0; u < N; ++u) {
+      const int o = 64 * (kg + KG * (i + u));
+      wa[u] = load16<ALIGNED>(rowA, o);
+#pragma unroll
+      for (int j = 0; j < CB; ++j) wb[u][j] = load16<ALIGNED>(rowP[j], o);
+    }
+    // the label of the lane's pattern in the argmax below, loaded behind
+    // the first operands so that its latency hides under the contraction
+    if (!YHAT && i == 0 && kg < 4 && mu < p.n) label = p.y[mu];
+#pragma unroll
+    for (int u = 0; u < N; ++u) {
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const uint4 ea = pm1_operand(wa[u], s);
+#pragma unroll
+        for (int j = 0; j < CB; ++j) acc[j] = mfma_fp4(ea, bit_operand(wb[u][j], s), acc[j], s);
+      }
+      if constexpr (YHAT) pa += popc_low(wa[u]);
+    }
+  };
+  int i = 0;
+  for (; i + CH <= nf; i += CH) run(std::integral_constant<int, CH>{}, i);
+  for (; i < nf; ++i) run(std::integral_constant<int, 1>{}, i);
+  if (!YHAT && nf == 0 && kg < 4 && mu < p.n) label = p.y[mu];
+  if (nsb > nfull && (nsb - 1) % KG == kg) {   // the super-block that holds K's end
+    const int sb = nsb - 1;
+    const uint4 a = load16_tail<ALIGNED>(rowA, 64 * sb, rowlim);
+    uint4 b[CB];
+#pragma unroll
+    for (int j = 0; j < CB; ++j) b[j] = load16_tail<ALIGNED>(rowP[j], 64 * sb, rowlim);
+    uint32_t valid[4];   // elements of word d before K
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      const int nv = K - (512 * sb + 128 * q + 32 * d);
+      valid[d] = nv >= 32 ? 0xFFFFFFFFu : nv <= 0 ? 0u : ((1u << nv) - 1u);
     }
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      const int t = tid + i * 64 * kWaves;
-      if (t < kLoads) *reinterpret_cast<uint4 *>(lds + (t / (kChunk / 4)) * kStride + (t % (kChunk / 4)) * 4) = v[i];
+    for (int s = 0; s < 4; ++s) {
+      const uint4 ea = pm1_operand(a, s);
+#pragma unroll
+      for (int j = 0; j < CB; ++j) acc[j] = mfma_fp4(ea, bit_operand_masked(b[j], valid, s), acc[j], s);
     }
-    __syncthreads();
-    const int nsteps = min(kChunk, w32 - kw0 + 3) / 4;   // K steps of 4 words in this chunk
-    if (cg * PB < nb && nsteps == kChunk / 4) {
-      // a whole chunk: every operand word of the wave's K steps is read
-      // from LDS first, so the reads overlap instead of queueing behind
-      // each step's MFMAs
-      constexpr int kSteps = kChunk / 4 / KG;
-      uint32_t wa[kSteps], wb[kSteps][PB];
-#pragma unroll
-      for (int s = 0; s < kSteps; ++s) {
-        const int wl = 4 * (kg + s * KG) + q;
-        wa[s] = sA[lr * kStride + wl];
-#pragma unroll
-        for (int j = 0; j < PB; ++j) wb[s][j] = sP[((cg * PB + j) * 16 + lr) * kStride + wl];
-      }
-#pragma unroll
-      for (int s = 0; s < kSteps; ++s) {
-        const int wl = 4 * (kg + s * KG) + q;
-        const int nv = min(max(Lr.K - 32 * (kw0 + wl), 0), 32);
-        const uint32_t valid = nv == 32 ? 0xFFFFFFFFu : ((1u << nv) - 1u);
-        const uint4 av = fp4x32_permuted(wa[s]);
-#pragma unroll
-        for (int j = 0; j < PB; ++j)
-          if (cg * PB + j < nb) {
-            const uint4 bv = valid == 0xFFFFFFFFu ? fp4x32_permuted(wb[s][j]) : fp4x32_permuted_masked(wb[s][j], valid);
-            acc[j] = mfma_fp4(av, bv, acc[j]);
-          }
-      }
-    } else if (cg * PB < nb) {   // the wave has a class block in range
-      for (int ks = kg; ks < nsteps; ks += KG) {
-        const int wl = 4 * ks + q;   // the lane's word of the step, in the chunk
-        // elements 32 (kw0 + wl) .. +31; those past K are padding (0 in fp4)
-        const int nv = min(max(Lr.K - 32 * (kw0 + wl), 0), 32);
-        const uint32_t valid = nv == 32 ? 0xFFFFFFFFu : ((1u << nv) - 1u);
-        const uint4 av = fp4x32_permuted(sA[lr * kStride + wl]);
-#pragma unroll
-        for (int j = 0; j < PB; ++j)
-          if (cg * PB + j < nb) {
-            const uint32_t bw = sP[((cg * PB + j) * 16 + lr) * kStride + wl];
-            const uint4 bv = valid == 0xFFFFFFFFu ? fp4x32_permuted(bw) : fp4x32_permuted_masked(bw, valid);
-            acc[j] = mfma_fp4(av, bv, acc[j]);
-          }
-      }
-    }
+    if constexpr (YHAT)
+      pa += __popc(a.x & kLowClasses & valid[0]) + __popc(a.y & kLowClasses & valid[1]) +
+            __popc(a.z & kLowClasses & valid[2]) + __popc(a.w & kLowClasses & valid[3]);
   }
-  __syncthreads();   // the staged chunk is no longer read: red reuses it
-  // lane holds classes (cg*PB + j)*16 + (lane & 15) of patterns
-  // 4*(lane >> 4) + e; blocks past nb are never read
+  // lane holds classes 16 j + lr of patterns 4q + e
 #pragma unroll
-  for (int j = 0; j < PB; ++j)
-    if (cg * PB + j < nb)
+  for (int j = 0; j < CB; ++j)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) red[kg][4 * (lane >> 4) + e][(cg * PB + j) * 16 + lr] = (int)acc[j][e];
-  __syncthreads();
-  for (int i = tid; i < 16 * CB * 16; i += 64 * kWaves) {
-    int sum = 0;
-#pragma unroll
-    for (int k = 0; k < KG; ++k) sum += (&red[k][0][0])[i];
-    (&red[0][0][0])[i] = sum;
+    for (int e = 0; e < 4; ++e) red[kg][4 * q + e][j * 16 + lr] = (int)acc[j][e];
+  if constexpr (YHAT) {
+    pa += __shfl_xor(pa, 16);
+    pa += __shfl_xor(pa, 32);
+    if (q == 0) spa[kg][lr] = pa;
   }
   __syncthreads();
-  if (p.mode == kClsYhatOnly) {
-    for (int i = tid; i < 16 * CB * 16; i += 64 * kWaves) {
-      const int r = i / (CB * 16), cl = i % (CB * 16);
-      const int m = m0 + r;
-      if (m < p.n && cl < p.c) Lr.yhat[(size_t)m * p.c + cl] = red[0][r][cl];
+  if constexpr (YHAT) {
+    const int nlow = K - K / 4;
+    for (int i = tid; i < 16 * p.c; i += 64 * kWaves) {
+      const int r = i / p.c, cl = i - r * p.c, m = m0 + r;
+      if (m < p.n) {
+        int v = 0, pr = 0;
+#pragma unroll
+        for (int k = 0; k < KG; ++k) {
+          v += red[k][r][cl];
+          pr += spa[k][r];
+        }
+        yhat_out[(size_t)m * p.c + cl] = v - 2 * pr + nlow;
+      }
     }
     return;
-  }
-  // Sixteen lanes per pattern (a DPP row): lane li scans classes li, li + 16,
-  // ... in order, then the row merges its lanes' top-two with four DPP
-  // exchanges (xor 1 and 2 within quads, then the half-row and row mirrors),
-  // after which every lane of the row holds the pattern's first argmax and
-  // its two largest values.  Waves 0..3 take the 16 patterns.
-  if (wave < 4) {
-    const int r = 4 * wave + (lane >> 4), li = lane & 15;
-    const int mu = m0 + r;
-    if (mu < p.n) {
-      Top2 t{INT_MIN, INT_MAX, INT_MIN};
-      for (int cl = li; cl < p.c; cl += 16) {
-        const int v = red[0][r][cl];
-        if (v > t.v1) {
-          t.v2 = t.v1;
-          t.v1 = v;
-          t.i1 = cl;
-        } else if (v > t.v2) {
-          t.v2 = v;
-        }
+  } else {
+    // Sixteen lanes per pattern (a DPP row): lane li takes classes li, li +
+    // 16, ... in order (the K groups' partials added), then the row merges
+    // its lanes' top-two with four DPP exchanges (xor 1 and 2 within quads,
+    // then the half-row and row mirrors), after which every lane of the row
+    // holds the pattern's first argmax and its two largest values.  Waves
+    // 0..3 take the 16 patterns.
+    if (kg < 4 && mu < p.n) {
+      const int r = mu - m0, li = lane & 15;
+      int v[CB];
+#pragma unroll
+      for (int j = 0; j < CB; ++j) {   // every LDS read first (entries past c are read, not used)
+        v[j] = 0;
+#pragma unroll
+        for (int k = 0; k < KG; ++k) v[j] += red[k][r][li + 16 * j];
       }
+      Top2 t{INT_MIN, INT_MAX, INT_MIN};
+#pragma unroll
+      for (int j = 0; j < CB; ++j)
+        if (li + 16 * j < p.c) {
+          if (v[j] > t.v1) {
+            t.v2 = t.v1;
+            t.v1 = v[j];
+            t.i1 = li + 16 * j;
+          } else if (v[j] > t.v2) {
+            t.v2 = v[j];
+          }
+        }
       t = merge(t, dpp_top2<0xB1>(t));    // quad_perm [1,0,3,2]
       t = merge(t, dpp_top2<0x4E>(t));    // quad_perm [2,3,0,1]
       t = merge(t, dpp_top2<0x141>(t));   // row_half_mirror
       t = merge(t, dpp_top2<0x140>(t));   // row_mirror
       if (li == 0) {
-        const int label = p.y[mu];
-        if (p.mode == kClsEval) {
+        if (mode == kClsEval) {
           if (t.i1 == label) atomicAdd(&cnt[2], 1);
-          if (Lr.flag != nullptr)
-            Lr.flag[mu] = (uint8_t)((t.i1 == label ? 1 : 0) | ((t.v1 - t.v2) >= Lr.thr ? 2 : 0));
+          if (flag_out != nullptr)
+            flag_out[mu] = (uint8_t)((t.i1 == label ? 1 : 0) | ((t.v1 - t.v2) >= thr ? 2 : 0));
         } else {
           const bool err = t.i1 != label;
-          const bool upd = err || (t.v1 - t.v2) < Lr.thr;
-          Lr.err[mu] = err ? 1 : 0;
-          Lr.upd[mu] = upd ? 1 : 0;
+          const bool upd = err || (t.v1 - t.v2) < thr;
+          err_out[mu] = err ? 1 : 0;
+          upd_out[mu] = upd ? 1 : 0;
           if (err) atomicAdd(&cnt[0], 1);
           if (upd) atomicAdd(&cnt[1], 1);
         }
       }
     }
-  }
-  // one global atomic per work-group (same-address atomics from every
-  // pattern would serialise in L2): err and |M| are adjacent 32-bit counts of
-  // the layer's stats row, added at once as one 64-bit value
-  __syncthreads();
-  if (tid == 0) {
-    if (p.mode == kClsEval) {
-      if (cnt[2]) atomicAdd(Lr.correct, cnt[2]);
-    } else {
-      const unsigned long long v = (unsigned long long)(uint32_t)cnt[0] | ((unsigned long long)(uint32_t)cnt[1] << 32);
-      if (v) atomicAdd(reinterpret_cast<unsigned long long *>(Lr.stats), v);
+    // one global atomic per work-group (same-address atomics from every
+    // pattern would serialise in L2): err and |M| are adjacent 32-bit counts
+    // of the layer's stats row, added at once as one 64-bit value
+    __syncthreads();
+    if (tid == 0) {
+      if (mode == kClsEval) {
+        if (cnt[2]) atomicAdd(correct_out, cnt[2]);
+      } else {
+        const unsigned long long v = (unsigned long long)(uint32_t)cnt[0] | ((unsigned long long)(uint32_t)cnt[1] << 32);
+        if (v) atomicAdd(reinterpret_cast<unsigned long long *>(stats_out), v);
+      }
     }
   }
 }
@@ -341,21 +399,52 @@ __global__ __launch_bounds__(64 * kArgWaves) void cls_argmax_kernel(ClsBatch p) 
   }
 }
 
+template <int CB>
+void launch_cls_cb(const ClsBatch &a, bool aligned, bool yhat, dim3 grid, hipStream_t s) {
+  const dim3 block(64 * kWaves);
+  if (aligned) {
+    if (yhat)
+      hipLaunchKernelGGL((cls_fp4_kernel<CB, true, true>), grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL((cls_fp4_kernel<CB, true, false>), grid, block, 0, s, a);
+  } else {
+    if (yhat)
+      hipLaunchKernelGGL((cls_fp4_kernel<CB, false, true>), grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL((cls_fp4_kernel<CB, false, false>), grid, block, 0, s, a);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_cls_fp4(const ClsBatch &a, hipStream_t s) {
   if (a.n <= 0 || a.nl <= 0) return hipSuccess;
   if (a.c < 1 || a.c > kClsMaxClasses || a.nl > kMaxClsLayers) return hipErrorInvalidValue;
-  const int nblk = (a.c + 15) / 16;
-  const dim3 grid(a.nl * ((a.n + 15) / 16)), block(64 * kWaves);
-  if (nblk <= 1)
-    hipLaunchKernelGGL(cls_fp4_kernel<1>, grid, block, 0, s, a);
-  else if (nblk <= 2)
-    hipLaunchKernelGGL(cls_fp4_kernel<2>, grid, block, 0, s, a);
-  else if (nblk <= 4)
-    hipLaunchKernelGGL(cls_fp4_kernel<4>, grid, block, 0, s, a);
-  else
-    hipLaunchKernelGGL(cls_fp4_kernel<8>, grid, block, 0, s, a);
+  const bool yhat = a.mode == kClsYhatOnly;
+  bool aligned = true;
+  for (int l = 0; l < a.nl; ++l) {
+    const ClsLayer &L = a.L[l];
+    if (L.A == nullptr || L.P == nullptr || L.K < 1 || L.words < (L.K + 63) / 64) return hipErrorInvalidValue;
+    if (yhat ? L.yhat == nullptr
+             : (a.mode == kClsEval ? L.correct == nullptr : (L.err == nullptr || L.upd == nullptr || L.stats == nullptr)))
+      return hipErrorInvalidValue;
+    // rows start on 16-byte boundaries when the bases are 16-byte aligned
+    // and the stride is an even number of words
+    aligned = aligned && L.words % 2 == 0 && (reinterpret_cast<uintptr_t>(L.A) & 15) == 0 &&
+              (reinterpret_cast<uintptr_t>(L.P) & 15) == 0;
+  }
+  if (!yhat && a.y == nullptr) return hipErrorInvalidValue;
+  const dim3 grid(a.nl * ((a.n + 15) / 16));
+  switch ((a.c + 15) / 16) {   // class blocks
+    case 1: launch_cls_cb<1>(a, aligned, yhat, grid, s); break;
+    case 2: launch_cls_cb<2>(a, aligned, yhat, grid, s); break;
+    case 3: launch_cls_cb<3>(a, aligned, yhat, grid, s); break;
+    case 4: launch_cls_cb<4>(a, aligned, yhat, grid, s); break;
+    case 5: launch_cls_cb<5>(a, aligned, yhat, grid, s); break;
+    case 6: launch_cls_cb<6>(a, aligned, yhat, grid, s); break;
+    case 7: launch_cls_cb<7>(a, aligned, yhat, grid, s); break;
+    default: launch_cls_cb<8>(a, aligned, yhat, grid, s); break;
+  }
   return hipGetLastError();
 }
 

@@ -98,30 +98,15 @@ __device__ __forceinline__ int swz(int r) { return (r >> 2) & 3; }
 // lane l: A row / B column (l & 31), half (l >> 5) of the 64-element K
 // block; result element i of lane l is row 8*(i>>2) + 4*(l>>5) + (i&3),
 // column (l & 31)
-// K classes.  Element k of a bit row is in class k mod 4: bit s = k mod 4
-// of nibble t of its 32-bit word (the word holds elements 4t + s).  The
-// MFMA of class s over a 256-element chunk takes, from each of the lane's
-// four words, the bits of class s in place (nibble t of dword d = bit 4t + s
-// of word d); A and B use the same map, so every product pairs the same k.
-//   * class 3 is the e2m1 sign bit: bit 1 -> 0x2 (+1), bit 0 -> 0xA (-1),
-//     one v_bitop3; its MFMA adds z_3 = sum over class-3 k of a_k w_k;
-//   * classes 0..2 keep the bit alone (one AND): 0 or 2^(s-1) (0.5, 1, 2);
-//     with block scales 2^(2-s) on both operands the MFMA adds 4 for every
-//     k where both bits are 1.
-// So acc = z_3 + 4 C, C = #{k in classes 0..2: a-bit = w-bit = 1}, and
-// z = acc + n_low - 2 (P_a + P_w), where P_a and P_w are the rows'
-// popcounts over classes 0..2 and n_low = K - floor(K / 4) the class 0..2
-// elements of a row.  Every value is an integer below 2^24: exact in fp32.
-__device__ __forceinline__ uint32_t class_bits(uint32_t w, int s) {
-  return s == 3 ? fp4_sign_nibbles(w) : (w & (0x11111111u << s));
-}
+// K classes (class_bits): the MFMA of class s over a 256-element chunk takes,
+// from each of the lane's four words, the bits of class s in place (nibble t
+// of dword d = bit 4t + s of word d); A and B use the same map, so every
+// product pairs the same k.  So acc = z_3 + 4 C, and z = acc + n_low -
+// 2 (P_a + P_w), where P_a and P_w are the rows' popcounts over classes 0..2
+// and n_low = K - floor(K / 4) the class 0..2 elements of a row.  Every
+// value is an integer below 2^24: exact in fp32.
 __device__ __forceinline__ uint4 class_operand(const uint4 &w, int s) {
   return make_uint4(class_bits(w.x, s), class_bits(w.y, s), class_bits(w.z, s), class_bits(w.w, s));
-}
-// the elements whose bit in valid is 0 become fp4 zeros (past K)
-__device__ __forceinline__ uint32_t class_bits_masked(uint32_t w, uint32_t valid, int s) {
-  if (s == 3) return fp4_sign_nibbles(w) & (((valid & 0x88888888u) >> 3) * 0xFu);
-  return w & valid & (0x11111111u << s);
 }
 
 // lane l: A row / B column (l & 31), half (l >> 5) of the 64-element K
@@ -132,11 +117,10 @@ __device__ __forceinline__ v16f mfma_class(const uint4 &a, const uint4 &b, v16f 
   const v8i bv = {(int)b.x, (int)b.y, (int)b.z, (int)b.w, 0, 0, 0, 0};
   // operand formats 4 = e2m1 for A and B; E8M0 block scales 2^(2-s) for
   // classes 0..2 (129, 128, 127), 1 for the sign class
-  const int sc = s == 0 ? 129 : s == 1 ? 128 : 127;
+  const int sc = class_scale(s);
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, c, 4, 4, 0, sc, 0, sc);
 }
 
-constexpr uint32_t kLowClasses = 0x77777777u;   // the bits of classes 0..2
 
 // one reduce-scatter step at lane distance D, the partner given by DPP
 // control CTRL: rows k + D move into slot k on lanes with bit D set
