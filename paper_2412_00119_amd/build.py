@@ -26,7 +26,8 @@ COMMON_FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-ffp-co
 # device code first, then the host code with that device code embedded, under
 # one compilation-unit id so that both passes name static device variables
 # alike.
-DEVICE_FLAGS = ["--offload-device-only", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+DEVICE_FLAGS = ["--offload-device-only", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-mllvm", "-amdgpu-kernarg-preload-count=16"]
 HOST_FLAGS = ["--offload-host-only"]
 
 

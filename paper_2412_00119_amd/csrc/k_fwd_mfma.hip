@@ -139,8 +139,15 @@ __device__ __forceinline__ void select_step(uint32_t (&v)[32], int lc) {
 // row starts on a 16-byte boundary, else 4.  SLICED: the launch covers
 // several layers (p.sl); a one-layer launch reads its fields directly, which
 // keeps the slice lookup out of its prologue.
+//
+// The arguments the first loads depend on come first, as separate scalars:
+// the leading 16 dwords of a kernel's arguments are preloaded into scalar
+// registers when the wave starts (kernarg preloading), so the tile's first
+// loads do not wait for a read of the argument buffer.
 template <int UNIT, bool SLICED>
-__global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
+__global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const uint64_t *pB, const int32_t *py, int pld,
+                                                      int pK, int pM, int pN, int pnt_m, int pnt_n, int pxcd,
+                                                      int pystride, int pmode, FwdArgs p) {
   // one LDS array per ring slot (A tile, then B tile): every access below
   // names its array, so the compiler can tell a slot being read from the
   // slots the direct-to-LDS loads are still filling (it tells apart at most
@@ -162,26 +169,26 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   FwdSlice S;   // a copy: kept in scalar registers
   int b = (int)blockIdx.x;
   if constexpr (SLICED) {
-    const int tiles = p.nt_m * p.nt_n;
+    const int tiles = pnt_m * pnt_n;
     const int sli = b / tiles;
     S = p.sl[sli];
     b -= sli * tiles;
   } else {
-    S = FwdSlice{p.A, p.B, p.lda, p.K, p.z, p.z32};
+    S = FwdSlice{pA, pB, pld, pK, p.z, p.z32};
   }
   int mt, nt;
   {
-    if (p.xcd_remap == 1) {   // XCD x takes the x-th eighth of B's tiles
-      const int x = b & 7, idx = b >> 3, per = p.nt_n >> 3;
-      nt = x * per + idx / p.nt_m;
-      mt = idx % p.nt_m;
-    } else if (p.xcd_remap == 2) {   // the x-th eighth of A's tiles
-      const int x = b & 7, idx = b >> 3, per = p.nt_m >> 3;
-      mt = x * per + idx / p.nt_n;
-      nt = idx % p.nt_n;
+    if (pxcd == 1) {   // XCD x takes the x-th eighth of B's tiles
+      const int x = b & 7, idx = b >> 3, per = pnt_n >> 3;
+      nt = x * per + idx / pnt_m;
+      mt = idx % pnt_m;
+    } else if (pxcd == 2) {   // the x-th eighth of A's tiles
+      const int x = b & 7, idx = b >> 3, per = pnt_m >> 3;
+      mt = x * per + idx / pnt_n;
+      nt = idx % pnt_n;
     } else {
-      nt = b / p.nt_m;
-      mt = b % p.nt_m;
+      nt = b / pnt_m;
+      mt = b % pnt_m;
     }
   }
   const int m0 = mt * TM, n0 = nt * TN;
@@ -201,7 +208,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   // selection is not fused the launcher points them at valid memory).
   const int pr = tid >> 1, pw = tid & 1;
   const int pm = m0 + pr, pwg = (n0 >> 6) + pw;
-  const bool pvalid = p.mode == kFwdFusedSelect && pm < p.M && pwg < p.words_out;
+  const bool pvalid = pmode == kFwdFusedSelect && pm < pM && pwg < p.words_out;
 
   // Loads: a wave moves rows 32*wave .. 32*wave+31 of each operand.  Lane l
   // of instruction h fills LDS bytes UNIT*l of its kRowsPerDma rows: row
@@ -218,8 +225,8 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
     const int r = 32 * wave + kRowsPerDma * h + pos / KB;
     const int inrow = pos % KB;
     offA[h] = 16 * ((inrow / 16) ^ swz(r)) + inrow % 16;
-    srcA[h] = reinterpret_cast<const uint8_t *>(S.A + (size_t)min(m0 + r, p.M - 1) * S.ld);
-    srcB[h] = reinterpret_cast<const uint8_t *>(S.B + (size_t)min(n0 + r, p.N - 1) * S.ld);
+    srcA[h] = reinterpret_cast<const uint8_t *>(S.A + (size_t)min(m0 + r, pM - 1) * S.ld);
+    srcB[h] = reinterpret_cast<const uint8_t *>(S.B + (size_t)min(n0 + r, pN - 1) * S.ld);
   }
   auto issue = [&](int ks, uint8_t *d) {
 #pragma unroll
@@ -367,7 +374,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(FwdArgs p) {
   if (wave == 0) {   // labels first: the oldest loads, covered by the prologue's wait
 #pragma unroll
     for (int h = 0; h < TM / 64; ++h)
-      dma<4>(p.y + (size_t)min(m0 + 64 * h + lane, p.M - 1) * p.ystride, sY + 64 * h);
+      dma<4>(py + (size_t)min(m0 + 64 * h + lane, pM - 1) * pystride, sY + 64 * h);
   }
   issue(0, s0);
   issue(min(1, klast), s1);
@@ -636,14 +643,17 @@ hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s) {
     a.pw_max = 0;
   }
   const dim3 grid(a.nslices * a.nt_m * a.nt_n);
+  const FwdSlice &s0 = a.sl[0];
+#define BMLP_FWD_ARGS s0.A, s0.B, a.y, s0.ld, s0.K, a.M, a.N, a.nt_m, a.nt_n, a.xcd_remap, a.ystride, a.mode, a
   if (aligned && sliced)
-    hipLaunchKernelGGL((fwd_fp4_kernel<16, true>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((fwd_fp4_kernel<16, true>), grid, dim3(256), 0, s, BMLP_FWD_ARGS);
   else if (aligned)
-    hipLaunchKernelGGL((fwd_fp4_kernel<16, false>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((fwd_fp4_kernel<16, false>), grid, dim3(256), 0, s, BMLP_FWD_ARGS);
   else if (sliced)
-    hipLaunchKernelGGL((fwd_fp4_kernel<4, true>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((fwd_fp4_kernel<4, true>), grid, dim3(256), 0, s, BMLP_FWD_ARGS);
   else
-    hipLaunchKernelGGL((fwd_fp4_kernel<4, false>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((fwd_fp4_kernel<4, false>), grid, dim3(256), 0, s, BMLP_FWD_ARGS);
+#undef BMLP_FWD_ARGS
   return hipGetLastError();
 }
 
