@@ -140,15 +140,18 @@ struct ClsShape {
 
 // ALIGNED: every row starts on a 16-byte boundary.  YHAT: y_hat is the
 // output (kClsYhatOnly); otherwise the error signal (kClsTrain, kClsEval).
+// The pattern count, the class count and the labels come first as scalars,
+// preloaded into scalar registers when the wave starts, so that the layer
+// lookup and the label loads do not wait for a read of the argument buffer.
 template <int CB, bool ALIGNED, bool YHAT>
-__global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
+__global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(int pn, int pc, const int32_t *py, ClsBatch p) {
   constexpr int KG = ClsShape<CB>::KG, CH = ClsShape<CB>::CH, LD = ClsShape<CB>::LD;
   __shared__ int red[KG][16][LD];        // y' partials of the K groups
   __shared__ int spa[KG][16];            // YHAT: P_a partials of the K groups
   __shared__ int cnt[3];                 // block totals of err, upd, correct
 
   const int tid = threadIdx.x, kg = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
-  const int bpl = (p.n + 15) / 16;               // work-groups per layer
+  const int bpl = (pn + 15) / 16;               // work-groups per layer
   const ClsLayer &Lr = p.L[blockIdx.x / bpl];
   const int m0 = (blockIdx.x % bpl) * 16;
   const int lr = lane & 15, q = lane >> 4;       // row / class, and which 16 bytes of a super-block
@@ -166,11 +169,11 @@ __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
                "s"(correct_out), "s"(yhat_out));
 
   // the lane's 16 bytes of each super-block start at row + 64 sb
-  const uint8_t *rowA = reinterpret_cast<const uint8_t *>(Lr.A + (size_t)min(m0 + lr, p.n - 1) * Lr.words) + 16 * q;
+  const uint8_t *rowA = reinterpret_cast<const uint8_t *>(Lr.A + (size_t)min(m0 + lr, pn - 1) * Lr.words) + 16 * q;
   const uint8_t *rowP[CB];
 #pragma unroll
   for (int j = 0; j < CB; ++j)
-    rowP[j] = reinterpret_cast<const uint8_t *>(Lr.P + (size_t)min(j * 16 + lr, p.c - 1) * Lr.words) + 16 * q;
+    rowP[j] = reinterpret_cast<const uint8_t *>(Lr.P + (size_t)min(j * 16 + lr, pc - 1) * Lr.words) + 16 * q;
   const int rowlim = 8 * Lr.words - 16 * q;      // bytes of the row from the lane's first byte
 
   v4f acc[CB];
@@ -197,7 +200,7 @@ __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
     }
     // the label of the lane's pattern in the argmax below, loaded behind
     // the first operands so that its latency hides under the contraction
-    if (!YHAT && i == 0 && kg < 4 && mu < p.n) label = p.y[mu];
+    if (!YHAT && i == 0 && kg < 4 && mu < pn) label = py[mu];
 #pragma unroll
     for (int u = 0; u < N; ++u) {
 #pragma unroll
@@ -212,7 +215,7 @@ __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
   int i = 0;
   for (; i + CH <= nf; i += CH) run(std::integral_constant<int, CH>{}, i);
   for (; i < nf; ++i) run(std::integral_constant<int, 1>{}, i);
-  if (!YHAT && nf == 0 && kg < 4 && mu < p.n) label = p.y[mu];
+  if (!YHAT && nf == 0 && kg < 4 && mu < pn) label = py[mu];
   if (nsb > nfull && (nsb - 1) % KG == kg) {   // the super-block that holds K's end
     const int sb = nsb - 1;
     const uint4 a = load16_tail<ALIGNED>(rowA, 64 * sb, rowlim);
@@ -248,16 +251,16 @@ __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
   __syncthreads();
   if constexpr (YHAT) {
     const int nlow = K - K / 4;
-    for (int i = tid; i < 16 * p.c; i += 64 * kWaves) {
-      const int r = i / p.c, cl = i - r * p.c, m = m0 + r;
-      if (m < p.n) {
+    for (int i = tid; i < 16 * pc; i += 64 * kWaves) {
+      const int r = i / pc, cl = i - r * pc, m = m0 + r;
+      if (m < pn) {
         int v = 0, pr = 0;
 #pragma unroll
         for (int k = 0; k < KG; ++k) {
           v += red[k][r][cl];
           pr += spa[k][r];
         }
-        yhat_out[(size_t)m * p.c + cl] = v - 2 * pr + nlow;
+        yhat_out[(size_t)m * pc + cl] = v - 2 * pr + nlow;
       }
     }
     return;
@@ -268,7 +271,7 @@ __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
     // then the half-row and row mirrors), after which every lane of the row
     // holds the pattern's first argmax and its two largest values.  Waves
     // 0..3 take the 16 patterns.
-    if (kg < 4 && mu < p.n) {
+    if (kg < 4 && mu < pn) {
       const int r = mu - m0, li = lane & 15;
       int v[CB];
 #pragma unroll
@@ -280,7 +283,7 @@ __global__ __launch_bounds__(64 * kWaves) void cls_fp4_kernel(ClsBatch p) {
       Top2 t{INT_MIN, INT_MAX, INT_MIN};
 #pragma unroll
       for (int j = 0; j < CB; ++j)
-        if (li + 16 * j < p.c) {
+        if (li + 16 * j < pc) {
           if (v[j] > t.v1) {
             t.v2 = t.v1;
             t.v1 = v[j];
@@ -404,14 +407,14 @@ void launch_cls_cb(const ClsBatch &a, bool aligned, bool yhat, dim3 grid, hipStr
   const dim3 block(64 * kWaves);
   if (aligned) {
     if (yhat)
-      hipLaunchKernelGGL((cls_fp4_kernel<CB, true, true>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((cls_fp4_kernel<CB, true, true>), grid, block, 0, s, a.n, a.c, a.y, a);
     else
-      hipLaunchKernelGGL((cls_fp4_kernel<CB, true, false>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((cls_fp4_kernel<CB, true, false>), grid, block, 0, s, a.n, a.c, a.y, a);
   } else {
     if (yhat)
-      hipLaunchKernelGGL((cls_fp4_kernel<CB, false, true>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((cls_fp4_kernel<CB, false, true>), grid, block, 0, s, a.n, a.c, a.y, a);
     else
-      hipLaunchKernelGGL((cls_fp4_kernel<CB, false, false>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((cls_fp4_kernel<CB, false, false>), grid, block, 0, s, a.n, a.c, a.y, a);
   }
 }
 

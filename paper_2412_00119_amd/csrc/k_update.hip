@@ -377,8 +377,15 @@ __device__ __host__ __forceinline__ int list_slots(int n, int gamma) { return ro
 // FULL: B = 2^M - 1 (B = 1, 3, 7, 15, 31, 63, 127), so u = B is every plane
 // set and u >= (B + 1) / 2 is the top plane; otherwise the planar
 // comparisons with the constants of B.
+// The layer lookup and the first load take their arguments from the
+// leading scalars, which are preloaded into scalar registers when the wave
+// starts: nl, the first work-group of layers 1..7 of the launch, and the
+// stats row of its layer 0 (the rows of the launch's layers follow it at
+// BMLP_STATS_STRIDE), so that |M_l| is requested before the argument
+// buffer has been read.
 template <int M, bool FULL>
-__global__ __launch_bounds__(kThreads, kSplit * kWaves / 4) void update_kernel(UpdateBatch p) {
+__global__ __launch_bounds__(kThreads, kSplit * kWaves / 4) void update_kernel(
+    int nl, int b1, int b2, int b3, int b4, int b5, int b6, int b7, const int32_t *stats0, UpdateBatch p) {
   extern __shared__ __align__(16) int smem[];
   __shared__ int wsum[kWaves];
   __shared__ int s_sel;
@@ -387,19 +394,31 @@ __global__ __launch_bounds__(kThreads, kSplit * kWaves / 4) void update_kernel(U
   // the wave index is uniform: in a scalar register, so are the item indices
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   // ---- which layer / group ---------------------------------------------------
+  const int bid = (int)blockIdx.x;
   int li = 0;
-#pragma unroll 1
-  for (int i = 1; i < p.nl; ++i)
-    if ((int)blockIdx.x >= p.L[i].block0) li = i;
+  li = (nl > 1 && bid >= b1) ? 1 : li;
+  li = (nl > 2 && bid >= b2) ? 2 : li;
+  li = (nl > 3 && bid >= b3) ? 3 : li;
+  li = (nl > 4 && bid >= b4) ? 4 : li;
+  li = (nl > 5 && bid >= b5) ? 5 : li;
+  li = (nl > 6 && bid >= b6) ? 6 : li;
+  li = (nl > 7 && bid >= b7) ? 7 : li;
+  const int mcount = stats0[li * BMLP_STATS_STRIDE + 1];
   const UpdLayer &U = p.L[li];
-  if (U.stats[1] == 0) return;   // M_l empty: Algorithm 2 is not run for this layer
-  const int g = ((int)blockIdx.x - U.block0) / kSplit;
-  const int part = ((int)blockIdx.x - U.block0) % kSplit;
-  const int gamma = U.gamma;
+  // what the bucketing reads first, requested together with |M_l| (one
+  // wait for both instead of a second round trip after the check)
+  const uint8_t *const upd = U.upd;
+  const int16_t *const kstar = U.kstar;
+  const int gamma = U.gamma, n = p.n, ldk = p.ldk;
+  asm volatile("" ::"s"(mcount), "s"(upd), "s"(kstar), "s"(gamma), "s"(n), "s"(ldk));
+  if (mcount == 0) return;   // M_l empty: Algorithm 2 is not run for this layer
+  const int block0 = li == 0 ? 0 : li == 1 ? b1 : li == 2 ? b2 : li == 3 ? b3 : li == 4 ? b4 : li == 5 ? b5 : li == 6 ? b6 : b7;
+  const int g = (bid - block0) / kSplit;
+  const int part = (bid - block0) % kSplit;
   // the selector list first (16-byte aligned), then the bucket offsets
   uint16_t *list = reinterpret_cast<uint16_t *>(smem);               // [list_slots(n, gamma)]
   int *bucket = smem + list_slots(p.n, gamma) / 2;                     // [gamma]
-  const int16_t *kcol = U.kstar + (size_t)g * p.ldk;
+  const int16_t *kcol = kstar + (size_t)g * ldk;
 
   // ---- bucket the selections of group g by perceptron (counting sort) -------
   if (tid == 0) s_sel = 0;
@@ -407,8 +426,8 @@ __global__ __launch_bounds__(kThreads, kSplit * kWaves / 4) void update_kernel(U
   __syncthreads();
   // U_l: the selections of the patterns in M_l
   int nsel = 0;
-  for (int mu = tid; mu < p.n; mu += kThreads) {
-    const int ks = U.upd[mu] ? kcol[mu] : -1;
+  for (int mu = tid; mu < n; mu += kThreads) {
+    const int ks = upd[mu] ? kcol[mu] : -1;
     if (ks >= 0) {
       atomicAdd(&bucket[ks], 1);
       ++nsel;
@@ -637,10 +656,14 @@ __global__ __launch_bounds__(kThreads, kSplit * kWaves / 4) void update_kernel(U
 
 template <int M>
 void launch_planes(bool full, dim3 grid, dim3 block, size_t lds, hipStream_t s, const UpdateBatch &b) {
+  int b0[kMaxUpdLayers] = {};
+  for (int i = 0; i < b.nl; ++i) b0[i] = b.L[i].block0;
+#define BMLP_UPD_ARGS b.nl, b0[1], b0[2], b0[3], b0[4], b0[5], b0[6], b0[7], b.L[0].stats, b
   if (full)
-    hipLaunchKernelGGL((update_kernel<M, true>), grid, block, lds, s, b);
+    hipLaunchKernelGGL((update_kernel<M, true>), grid, block, lds, s, BMLP_UPD_ARGS);
   else
-    hipLaunchKernelGGL((update_kernel<M, false>), grid, block, lds, s, b);
+    hipLaunchKernelGGL((update_kernel<M, false>), grid, block, lds, s, BMLP_UPD_ARGS);
+#undef BMLP_UPD_ARGS
 }
 
 }  // namespace
@@ -653,8 +676,12 @@ hipError_t launch_update(UpdateBatch &b, hipStream_t s) {
   if (b.n <= 0 || b.nl <= 0) return hipSuccess;
   int blocks = 0;
   int gmax = 0;
+  static_assert(kMaxUpdLayers == 8, "the kernel's leading arguments name layers 1..7");
+  if (b.nl > kMaxUpdLayers) return hipErrorInvalidValue;
   for (int i = 0; i < b.nl; ++i) {
     UpdLayer &u = b.L[i];
+    // the kernel finds the stats row of layer i at stats0 + i * BMLP_STATS_STRIDE
+    if (u.stats != b.L[0].stats + (size_t)i * BMLP_STATS_STRIDE) return hipErrorInvalidValue;
     u.chunks = (u.nw32 + 63) / 64;
     u.block0 = blocks;
     blocks += u.groups * kSplit;
