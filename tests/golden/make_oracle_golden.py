@@ -7,6 +7,8 @@ too slow to recompute inside a GPU test run, which is why they are stored.
 
     python tests/golden/make_oracle_golden.py small    # small_five_epochs.json
     python tests/golden/make_oracle_golden.py stress   # stress_step0_reinforced.txt
+    python tests/golden/make_oracle_golden.py headline # headline_24_steps.json
+    python tests/golden/make_oracle_golden.py field    # field_24_steps.json
 
 small: the 784 -> 1024 -> 1024 workload (10 classes, B = 127, batch 256,
 60 000 training and 10 000 held-out samples) over its five-epoch schedule:
@@ -21,6 +23,15 @@ correct, exit and correct-exit counts (early exit, Section 3.1).
 stress: the 8192 -> 8192 x 8 workload's first step (t = 0, p_r = 0.5): the
 number of reinforcement draws u < T_l over every hidden weight of each layer
 (Algorithm 3), the one step statistic a GPU test cannot afford to recompute.
+
+headline, field: the 3072 -> 4096 x 4 workload (100 classes, B = 31, batch
+1024) and the 3072 -> 2048 x 3 workload (10 classes, B = 127, batch 512) over
+their first 24 steps (t = 0 .. 23, p_r = 0.5, batch b of the training split's
+first 24 batches at step b): the steps where every pattern is in M_l and the
+ones after them where M_l has a few patterns and the update is mostly the
+reinforcement pass.  Per step and layer: the counts (01-loss, |M_l|, |U_l|,
+reinforced draws) and the SHA-256 of a_l (int8 ±1, [n][K_l], C order) and of
+H_l after the step (int8, [K_l][K_{l-1}], C order).
 """
 from __future__ import annotations
 
@@ -41,6 +52,9 @@ import oracle.bmlp as ob  # noqa: E402
 from paper_2412_00119_amd import synth  # noqa: E402
 
 SMALL_FILE = os.path.join(HERE, "small_five_epochs.json")
+RUN_FILES = {"headline": os.path.join(HERE, "headline_24_steps.json"),
+             "field": os.path.join(HERE, "field_24_steps.json")}
+RUN_STEPS = 24
 STRESS_FILE = os.path.join(HERE, "stress_step0_reinforced.txt")
 
 
@@ -102,7 +116,33 @@ def stress() -> None:
         f.write("\n".join(lines) + "\n")
 
 
+def steps_run(name: str) -> None:
+    w = {"headline": synth.HEADLINE, "field": synth.FIELD}[name]
+    cfg = ob.Config(w.widths, w.n_classes, w.bound, w.group_size, w.robustness, w.seed_model)
+    st = ob.init(cfg)
+    d = synth.make_split(w, "train", n=RUN_STEPS * w.batch)
+    steps = []
+    for t, (x, y) in enumerate(d.batches(w.batch)):
+        t0 = time.time()
+        tr = ob.train_step(st, x, y, t, w.p_r)
+        steps.append({
+            "t": t,
+            "stats": [lt.stats.astype(int).tolist() for lt in tr],
+            "a_sha256": [h_digest(lt.a) for lt in tr],
+            "h_sha256": [h_digest(st.H[l]) for l in range(cfg.n_layers)],
+        })
+        print(f"{name} step {t}: |M| {[int(lt.stats[1]) for lt in tr]} ({time.time() - t0:.0f} s)", flush=True)
+    out = {"workload": w.name, "widths": list(w.widths), "classes": w.n_classes, "bound": w.bound,
+           "batch": w.batch, "seed_model": w.seed_model, "robustness": w.robustness,
+           "group_size": w.group_size, "p_r": w.p_r.hex(), "steps": steps,
+           "made_by": f"python tests/golden/make_oracle_golden.py {name}"}
+    with open(RUN_FILES[name], "w") as f:
+        json.dump(out, f, indent=0)
+        f.write("\n")
+
+
 if __name__ == "__main__":
-    which = sys.argv[1:] or ["small", "stress"]
+    which = sys.argv[1:] or ["small", "stress", "headline", "field"]
     for name in which:
-        {"small": small, "stress": stress}[name]()
+        {"small": small, "stress": stress, "headline": lambda: steps_run("headline"),
+         "field": lambda: steps_run("field")}[name]()
