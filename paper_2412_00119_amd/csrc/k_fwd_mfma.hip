@@ -249,6 +249,13 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
     uint4 a[2][2], b[2][2];
   };
   const int arow = lane & 31, ahalf = lane >> 5;
+  // Register fragment i of a wave's A operands holds tile fragment i ^ wn
+  // (rows wm*64 + (i ^ wn)*32 ..): the A fragment a wave counts in the row
+  // popcounts below (fragment wn) is then always register fragment 0, with
+  // no select per word.  acc[i][j] holds tile rows of fragment i ^ wn.  (The
+  // same order for the B fragments by wm measured slower: the compiler then
+  // waits for every LDS read early in each K step.)
+  const int xa = wn;
   auto read = [&](Ops &o, const uint8_t *t) {
     const uint8_t *tA = t, *tB = t + TM * KB;
 #pragma unroll
@@ -256,7 +263,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
       const int u = 2 * c + ahalf;   // 16-byte unit of the 64-byte row
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        const int ra_ = wm * 64 + i * 32 + arow, rb_ = wn * 64 + i * 32 + arow;
+        const int ra_ = wm * 64 + (i ^ xa) * 32 + arow, rb_ = wn * 64 + i * 32 + arow;
         o.a[c][i] = *reinterpret_cast<const uint4 *>(&tA[ra_ * KB + ((u ^ swz(ra_)) * 16)]);
         o.b[c][i] = *reinterpret_cast<const uint4 *>(&tB[rb_ * KB + ((u ^ swz(rb_)) * 16)]);
       }
@@ -294,19 +301,16 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
   };
   // Row popcounts of classes 0..2 (P_a for the A rows, P_w for the B rows),
   // from the operand words the lanes already hold: wave (wm, wn) counts A
-  // fragment wn and B fragment wm, so every tile row and column is counted
-  // once, lane l over half (l >> 5) of the row (a wave-uniform branch picks
-  // the fragments: a select would cost a VALU instruction per word).  m[q]:
-  // the bits of word q of a chunk that count.
+  // fragment wn (its register fragment 0) and B fragment wm (picked by a
+  // wave-uniform branch, which the compiler turns into a select per word),
+  // so every tile row and column is counted once, lane l over half (l >> 5)
+  // of the row.  m[q]: the bits of word q of a chunk that count.
   uint32_t pca = 0u, pcb = 0u;
   auto popc4 = [](const uint4 &w, const uint32_t (&m)[4]) {
     return __popc(w.x & m[0]) + __popc(w.y & m[1]) + __popc(w.z & m[2]) + __popc(w.w & m[3]);
   };
   auto popc_ops = [&](const Ops &o, const uint32_t (&m0)[4], const uint32_t (&m1)[4]) {
-    if (wn == 0)
-      pca += popc4(o.a[0][0], m0) + popc4(o.a[1][0], m1);
-    else
-      pca += popc4(o.a[0][1], m0) + popc4(o.a[1][1], m1);
+    pca += popc4(o.a[0][0], m0) + popc4(o.a[1][0], m1);
     if (wm == 0)
       pcb += popc4(o.b[0][0], m0) + popc4(o.b[1][0], m1);
     else
@@ -327,10 +331,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
       uint32_t mv[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) mv[q] = valid[q] & kLowClasses;
-      if (wn == 0)
-        pca += popc4(o.a[c][0], mv);
-      else
-        pca += popc4(o.a[c][1], mv);
+      pca += popc4(o.a[c][0], mv);
       if (wm == 0)
         pcb += popc4(o.b[c][0], mv);
       else
@@ -468,7 +469,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
     float fa[2], fb[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
-      fa[i] = lh == 0 ? nlow - 2.f * (float)sPc[wm * 64 + i * 32 + lc] : 1.f;
+      fa[i] = lh == 0 ? nlow - 2.f * (float)sPc[wm * 64 + (i ^ xa) * 32 + lc] : 1.f;
 #pragma unroll
     for (int j = 0; j < 2; ++j)
       fb[j] = lh == 0 ? 1.f : -2.f * (float)sPc[TM + wn * 64 + j * 32 + lc];
@@ -498,7 +499,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
       }
   {
     const int i = lane >> 5, j = (lane >> 4) & 1, e = lane & 15;
-    const int rl0 = wm * 64 + i * 32 + 8 * (e >> 2) + (e & 3);   // the lanes-0-31 row; +4 for 32-63
+    const int rl0 = wm * 64 + (i ^ xa) * 32 + 8 * (e >> 2) + (e & 3);   // the lanes-0-31 row; +4 for 32-63
     const int cw = ((n0 + wn * 64) >> 5) + j;                      // 32-bit word of the 32 columns
     uint32_t *ab32 = reinterpret_cast<uint32_t *>(p.abits);
 #pragma unroll
@@ -531,7 +532,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
         for (int i = 0; i < 2; ++i)
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
-            const int rl = wm * 64 + i * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
+            const int rl = wm * 64 + (i ^ xa) * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
             const uint64_t rho = sP[wn][rl];
             uint32_t key[2];
 #pragma unroll
@@ -567,7 +568,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
       select_step<2, 0x4E>(v, lc);    // quad_perm [2,3,0,1]
       select_step<1, 0xB1>(v, lc);    // quad_perm [1,0,3,2]
       const int i = lc >> 4, e = lc & 15;
-      const int rl = wm * 64 + i * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
+      const int rl = wm * 64 + (i ^ xa) * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
       const int m = m0 + rl;
       if (m < p.M) p.kstar[(size_t)g * p.ldk + m] = (v[0] >= (1u << 27)) ? (int16_t)-1 : (int16_t)(v[0] & 0x3Fu);
     }
@@ -579,7 +580,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const int m = m0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
+          const int m = m0 + wm * 64 + (i ^ xa) * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
           const int col = n0 + wn * 64 + j * 32 + lc;
           if (m < p.M && col < p.N) {
             const size_t o = (size_t)m * p.ldz + col;
