@@ -121,7 +121,6 @@ __device__ __forceinline__ v16f mfma_class(const uint4 &a, const uint4 &b, v16f 
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, c, 4, 4, 0, sc, 0, sc);
 }
 
-
 // one reduce-scatter step at lane distance D, the partner given by DPP
 // control CTRL: rows k + D move into slot k on lanes with bit D set
 template <int D, int CTRL>
