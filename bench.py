@@ -62,23 +62,23 @@ def update_bytes(w):
     return tot
 
 
-def source_sha256(rel):
-    import hashlib
-    with open(os.path.join(ROOT, rel), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+def build_sha256(rel):
+    from paper_2412_00119_amd.build import kernel_fingerprint
+    return kernel_fingerprint(os.path.join(ROOT, rel))
 
 
 def measured_traffic(kernel, workload):
     """HBM bytes per launch of `kernel` from the committed counter summary,
-    or None when there is none or the kernel source changed since."""
+    or None when there is none or the kernel source or its device compile
+    flags changed since."""
     import re
     path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
-    m_sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
+    m_sha = re.search(r"kernel_build_sha256:\s*([0-9a-f]{64})", text)
     m_b = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    if not m_sha or not m_b or m_sha.group(1) != source_sha256(FWD_SOURCES[kernel]):
+    if not m_sha or not m_b or m_sha.group(1) != build_sha256(FWD_SOURCES[kernel]):
         return None
     return float(m_b.group(1))
 

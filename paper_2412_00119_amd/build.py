@@ -6,6 +6,7 @@ this file.  The C ABI is declared in include/bmlp.h at the repository root.
 from __future__ import annotations
 
 import glob
+import hashlib
 import os
 import shutil
 import subprocess
@@ -26,9 +27,23 @@ COMMON_FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-ffp-co
 # device code first, then the host code with that device code embedded, under
 # one compilation-unit id so that both passes name static device variables
 # alike.
+# MFMA accumulators in ordinary VGPRs instead of AGPRs: the epilogues read
+# every accumulator with VALU instructions (ballots, keys, argmax), which
+# otherwise copy each one out of the AGPRs first (v_accvgpr_read).
 DEVICE_FLAGS = ["--offload-device-only", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-                "-mllvm", "-amdgpu-kernarg-preload-count=16"]
+                "-mllvm", "-amdgpu-kernarg-preload-count=16", "-mllvm", "-amdgpu-mfma-vgpr-form"]
 HOST_FLAGS = ["--offload-host-only"]
+
+
+def kernel_fingerprint(src: str) -> str:
+    """SHA-256 of a kernel source and of the flags its device code is
+    compiled with: a counter profile taken from another build of the kernel no
+    longer describes it."""
+    h = hashlib.sha256()
+    with open(src, "rb") as f:
+        h.update(f.read())
+    h.update(b"\0" + " ".join(COMMON_FLAGS + DEVICE_FLAGS).encode())
+    return h.hexdigest()
 
 
 def hipcc() -> str:

@@ -13,8 +13,9 @@ WRITE_SIZE counters (KiB per dispatch, from two separate `--pmc` runs), finds
 the calibration copy (the largest `copyBuffer` dispatch, a plain
 device-to-device copy of N bytes each way), derives the factor that maps each
 counter onto the copy's known bytes, and reports the scaled bytes per launch
-of the kernels matching REGEX with the SHA-256 of their source file, so that a
-reader can tell whether the figure still describes the current kernel.
+of the kernels matching REGEX with the SHA-256 of their source file and device
+compile flags, so that a reader can tell whether the figure still describes the
+current kernel.
 """
 from __future__ import annotations
 
@@ -22,7 +23,6 @@ import argparse
 import collections
 import csv
 import glob
-import hashlib
 import os
 import re
 import sys
@@ -82,8 +82,8 @@ def traffic(args) -> None:
         if not ker:
             sys.exit(f"{counter}: no dispatch of {args.kernel} in {dirname}")
         out[counter] = (factor, calib_kib, sum(ker) / len(ker), len(ker))
-    with open(args.source, "rb") as f:
-        sha = hashlib.sha256(f.read()).hexdigest()
+    from paper_2412_00119_amd.build import kernel_fingerprint
+    sha = kernel_fingerprint(args.source)
     fetch_f, fetch_c, fetch_kib, n_f = out["FETCH_SIZE"]
     write_f, write_c, write_kib, n_w = out["WRITE_SIZE"]
     fetch_b = fetch_kib * 1024.0 * fetch_f
@@ -101,7 +101,7 @@ def traffic(args) -> None:
     print(f"| WRITE_SIZE | {write_c:.0f} | {write_f:.3f} | {write_kib:.1f} | {n_w} | {write_b:.4g} |")
     print(f"\ncalibration copy: {args.calib_bytes} bytes read and {args.calib_bytes} bytes written\n")
     print(f"kernel_source: {os.path.relpath(args.source)}")
-    print(f"kernel_source_sha256: {sha}")
+    print(f"kernel_build_sha256: {sha}")
     print(f"fetch_bytes_per_launch: {fetch_b:.6g}")
     print(f"write_bytes_per_launch: {write_b:.6g}")
     print(f"traffic_bytes_per_launch: {fetch_b + write_b:.6g}")
