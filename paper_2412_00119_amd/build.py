@@ -29,9 +29,12 @@ COMMON_FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-ffp-co
 # alike.
 # MFMA accumulators in ordinary VGPRs instead of AGPRs: the epilogues read
 # every accumulator with VALU instructions (ballots, keys, argmax), which
-# otherwise copy each one out of the AGPRs first (v_accvgpr_read).
+# otherwise copy each one out of the AGPRs first (v_accvgpr_read).  Wave
+# priority raised until a wave's first memory loads are issued (s_setprio),
+# so that the update kernel's six waves per SIMD start their loads early.
 DEVICE_FLAGS = ["--offload-device-only", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-                "-mllvm", "-amdgpu-kernarg-preload-count=16", "-mllvm", "-amdgpu-mfma-vgpr-form"]
+                "-mllvm", "-amdgpu-kernarg-preload-count=16", "-mllvm", "-amdgpu-mfma-vgpr-form",
+                "-mllvm", "-amdgpu-set-wave-priority"]
 HOST_FLAGS = ["--offload-host-only"]
 
 
