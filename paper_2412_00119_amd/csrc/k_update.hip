@@ -45,6 +45,7 @@ namespace {
 constexpr int kWaves = 12;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kSplit = 2;
+constexpr int kPre = 2;   // patterns per thread whose selection data the prologue loads up front
 constexpr int kPlanes = 15;   // counts up to 2^15 - 1 >= BMLP_MAX_BATCH
 
 // A wave-uniform word the compiler must treat as unknown and keep in a
@@ -409,16 +410,32 @@ __global__ __launch_bounds__(kThreads, kSplit * kWaves / 4) void update_kernel(
   // wait for both instead of a second round trip after the check)
   const uint8_t *const upd = U.upd;
   const int16_t *const kstar = U.kstar;
+  const int32_t *const labels = p.y;
   const int gamma = U.gamma, n = p.n, ldk = p.ldk;
-  asm volatile("" ::"s"(mcount), "s"(upd), "s"(kstar), "s"(gamma), "s"(n), "s"(ldk));
-  if (mcount == 0) return;   // M_l empty: Algorithm 2 is not run for this layer
+  asm volatile("" ::"s"(mcount), "s"(upd), "s"(kstar), "s"(labels), "s"(gamma), "s"(n), "s"(ldk));
   const int block0 = li == 0 ? 0 : li == 1 ? b1 : li == 2 ? b2 : li == 3 ? b3 : li == 4 ? b4 : li == 5 ? b5 : li == 6 ? b6 : b7;
   const int g = (bid - block0) / kSplit;
   const int part = (bid - block0) % kSplit;
+  const int16_t *kcol = kstar + (size_t)g * ldk;
+  // The first kPre patterns of each thread: M_l flag, k* and label loaded
+  // before |M_l| is known (in bounds: the index is clamped), so that they
+  // arrive with it, and kept for the list fill below, which then loads only
+  // the word of P_l that holds the selection's rho bit.
+  int ks_pre[kPre], y_pre[kPre];
+#pragma unroll
+  for (int q = 0; q < kPre; ++q) {
+    const int mu = tid + q * kThreads, muc = min(mu, n - 1);
+    const int f = upd[muc], k16 = kcol[muc];
+    y_pre[q] = labels[muc];
+    ks_pre[q] = (mu < n && f) ? k16 : -1;
+  }
+  // used before the check, so that the compiler keeps the loads above it
+  static_assert(kPre == 2, "one use of every preloaded value");
+  asm volatile("" ::"v"(ks_pre[0]), "v"(y_pre[0]), "v"(ks_pre[1]), "v"(y_pre[1]));
+  if (mcount == 0) return;   // M_l empty: Algorithm 2 is not run for this layer
   // the selector list first (16-byte aligned), then the bucket offsets
   uint16_t *list = reinterpret_cast<uint16_t *>(smem);               // [list_slots(n, gamma)]
   int *bucket = smem + list_slots(p.n, gamma) / 2;                     // [gamma]
-  const int16_t *kcol = kstar + (size_t)g * ldk;
 
   // ---- bucket the selections of group g by perceptron (counting sort) -------
   if (tid == 0) s_sel = 0;
@@ -426,7 +443,13 @@ __global__ __launch_bounds__(kThreads, kSplit * kWaves / 4) void update_kernel(
   __syncthreads();
   // U_l: the selections of the patterns in M_l
   int nsel = 0;
-  for (int mu = tid; mu < n; mu += kThreads) {
+#pragma unroll
+  for (int q = 0; q < kPre; ++q)
+    if (ks_pre[q] >= 0) {
+      atomicAdd(&bucket[ks_pre[q]], 1);
+      ++nsel;
+    }
+  for (int mu = tid + kPre * kThreads; mu < n; mu += kThreads) {
     const int ks = upd[mu] ? kcol[mu] : -1;
     if (ks >= 0) {
       atomicAdd(&bucket[ks], 1);
@@ -464,15 +487,19 @@ __global__ __launch_bounds__(kThreads, kSplit * kWaves / 4) void update_kernel(
   }
   __syncthreads();
   if (!p.sequential) {
-    for (int mu = tid; mu < p.n; mu += kThreads) {
+    auto fill = [&](int mu, int ks, int y) {
+      const int k = U.perm ? U.perm[g * gamma + ks] : g * gamma + ks;
+      const int yl = min(max(y, 0), p.c - 1);   // stay inside P on a bad label
+      const bool rpos = (U.P[(size_t)yl * U.words_out + (k >> 6)] >> (k & 63)) & 1ull;
+      const int pos = atomicAdd(&bucket[ks], 1);
+      list[pos] = (uint16_t)(mu | (rpos ? 0 : 0x8000));
+    };
+#pragma unroll
+    for (int q = 0; q < kPre; ++q)
+      if (ks_pre[q] >= 0) fill(tid + q * kThreads, ks_pre[q], y_pre[q]);
+    for (int mu = tid + kPre * kThreads; mu < p.n; mu += kThreads) {
       const int ks = U.upd[mu] ? kcol[mu] : -1;
-      if (ks >= 0) {
-        const int k = U.perm ? U.perm[g * gamma + ks] : g * gamma + ks;
-        const int yl = min(max(p.y[mu], 0), p.c - 1);   // stay inside P on a bad label
-        const bool rpos = (U.P[(size_t)yl * U.words_out + (k >> 6)] >> (k & 63)) & 1ull;
-        const int pos = atomicAdd(&bucket[ks], 1);
-        list[pos] = (uint16_t)(mu | (rpos ? 0 : 0x8000));
-      }
+      if (ks >= 0) fill(mu, ks, p.y[mu]);
     }
   } else if (wave == 0) {
     // the same lists, each in pattern order: wave 0 walks the patterns 64
