@@ -121,6 +121,13 @@ __device__ __forceinline__ v16f mfma_class(const uint4 &a, const uint4 &b, v16f 
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, c, 4, 4, 0, sc, 0, sc);
 }
 
+// acc + popcount(x) in one v_bcnt_u32_b32
+__device__ __forceinline__ uint32_t bcnt_acc(uint32_t x, uint32_t acc) {
+  uint32_t r;
+  asm("v_bcnt_u32_b32 %0, %1, %2" : "=v"(r) : "v"(x), "v"(acc));
+  return r;
+}
+
 // one reduce-scatter step at lane distance D, the partner given by DPP
 // control CTRL: rows k + D move into slot k on lanes with bit D set
 template <int D, int CTRL>
@@ -300,20 +307,24 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
   };
   // Row popcounts of classes 0..2 (P_a for the A rows, P_w for the B rows),
   // from the operand words the lanes already hold: wave (wm, wn) counts A
-  // fragment wn (its register fragment 0) and B fragment wm (picked by a
-  // wave-uniform branch, which the compiler turns into a select per word),
+  // fragment wn (its register fragment 0) and B fragment wm (one select per
+  // word, on the wave-uniform wm),
   // so every tile row and column is counted once, lane l over half (l >> 5)
   // of the row.  m[q]: the bits of word q of a chunk that count.
   uint32_t pca = 0u, pcb = 0u;
-  auto popc4 = [](const uint4 &w, const uint32_t (&m)[4]) {
-    return __popc(w.x & m[0]) + __popc(w.y & m[1]) + __popc(w.z & m[2]) + __popc(w.w & m[3]);
+  // each word's count added straight into the running total: left to
+  // itself the compiler counts every word from zero and sums the counts
+  // with three-input adds, half an instruction more per word
+  auto popc4 = [](uint32_t acc, const uint4 &w, const uint32_t (&m)[4]) {
+    acc = bcnt_acc(w.x & m[0], acc);
+    acc = bcnt_acc(w.y & m[1], acc);
+    acc = bcnt_acc(w.z & m[2], acc);
+    return bcnt_acc(w.w & m[3], acc);
   };
   auto popc_ops = [&](const Ops &o, const uint32_t (&m0)[4], const uint32_t (&m1)[4]) {
-    pca += popc4(o.a[0][0], m0) + popc4(o.a[1][0], m1);
-    if (wm == 0)
-      pcb += popc4(o.b[0][0], m0) + popc4(o.b[1][0], m1);
-    else
-      pcb += popc4(o.b[0][1], m0) + popc4(o.b[1][1], m1);
+    pca = popc4(popc4(pca, o.a[0][0], m0), o.a[1][0], m1);
+    const uint4 b0 = wm == 0 ? o.b[0][0] : o.b[0][1], b1 = wm == 0 ? o.b[1][0] : o.b[1][1];
+    pcb = popc4(popc4(pcb, b0, m0), b1, m1);
   };
   const uint32_t kFull[4] = {kLowClasses, kLowClasses, kLowClasses, kLowClasses};
   // the last step when K is not a multiple of 512: elements past K become
@@ -330,11 +341,8 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
       uint32_t mv[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) mv[q] = valid[q] & kLowClasses;
-      pca += popc4(o.a[c][0], mv);
-      if (wm == 0)
-        pcb += popc4(o.b[c][0], mv);
-      else
-        pcb += popc4(o.b[c][1], mv);
+      pca = popc4(pca, o.a[c][0], mv);
+      pcb = popc4(pcb, wm == 0 ? o.b[c][0] : o.b[c][1], mv);
 #pragma unroll
       for (int cls = 0; cls < 4; ++cls) {
         uint4 ea[2], eb[2];
