@@ -253,6 +253,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
   // lane (r, h) holds elements 256 c + 128 h .. +127 of row r
   struct Ops {
     uint4 a[2][2], b[2][2];
+    uint4 bc[2];   // the B fragment this wave counts (fragment wm), per chunk
   };
   const int arow = lane & 31, ahalf = lane >> 5;
   // Register fragment i of a wave's A operands holds tile fragment i ^ wn
@@ -273,6 +274,8 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
         o.a[c][i] = *reinterpret_cast<const uint4 *>(&tA[ra_ * KB + ((u ^ swz(ra_)) * 16)]);
         o.b[c][i] = *reinterpret_cast<const uint4 *>(&tB[rb_ * KB + ((u ^ swz(rb_)) * 16)]);
       }
+      const int rc_ = wn * 64 + wm * 32 + arow;
+      o.bc[c] = *reinterpret_cast<const uint4 *>(&tB[rc_ * KB + ((u ^ swz(rc_)) * 16)]);
     }
   };
   // The expanded operands of one K block (c, q) of a step.  A step's MFMAs
@@ -306,9 +309,10 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
     }
   };
   // Row popcounts of classes 0..2 (P_a for the A rows, P_w for the B rows),
-  // from the operand words the lanes already hold: wave (wm, wn) counts A
-  // fragment wn (its register fragment 0) and B fragment wm (one select per
-  // word, on the wave-uniform wm),
+  // from operand words the lanes read anyway: wave (wm, wn) counts A
+  // fragment wn (its register fragment 0) and B fragment wm (read from LDS
+  // a second time, into bc, the choice made in the address: two more LDS
+  // reads per step instead of a select per word),
   // so every tile row and column is counted once, lane l over half (l >> 5)
   // of the row.  m[q]: the bits of word q of a chunk that count.
   uint32_t pca = 0u, pcb = 0u;
@@ -323,8 +327,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
   };
   auto popc_ops = [&](const Ops &o, const uint32_t (&m0)[4], const uint32_t (&m1)[4]) {
     pca = popc4(popc4(pca, o.a[0][0], m0), o.a[1][0], m1);
-    const uint4 b0 = wm == 0 ? o.b[0][0] : o.b[0][1], b1 = wm == 0 ? o.b[1][0] : o.b[1][1];
-    pcb = popc4(popc4(pcb, b0, m0), b1, m1);
+    pcb = popc4(popc4(pcb, o.bc[0], m0), o.bc[1], m1);
   };
   const uint32_t kFull[4] = {kLowClasses, kLowClasses, kLowClasses, kLowClasses};
   // the last step when K is not a multiple of 512: elements past K become
@@ -342,7 +345,7 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
 #pragma unroll
       for (int q = 0; q < 4; ++q) mv[q] = valid[q] & kLowClasses;
       pca = popc4(pca, o.a[c][0], mv);
-      pcb = popc4(pcb, wm == 0 ? o.b[c][0] : o.b[c][1], mv);
+      pcb = popc4(pcb, o.bc[c], mv);
 #pragma unroll
       for (int cls = 0; cls < 4; ++cls) {
         uint4 ea[2], eb[2];
@@ -412,12 +415,12 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
     // The order of the step's instructions: each MFMA followed by a quarter
     // of the next K block's operands, so that the VALU work runs while the
     // matrix core works on the MFMA; one LDS read after each of the first
-    // eight MFMAs (issued before them, the reads would share the wait-count
+    // ten MFMAs (issued before them, the reads would share the wait-count
     // of the operands being consumed).
 #pragma unroll
     for (int i = 0; i < 32; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-      if (i < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+      if (i < 10) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
       __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);   // VALU
     }
     __builtin_amdgcn_sched_barrier(0);
