@@ -19,6 +19,12 @@ enum : uint32_t {
   kStreamGroups = 6,    // per-step group order (reshuffle variant)
 };
 
+// The fourth word of a buffer descriptor for a raw (stride 0) buffer of
+// 32-bit words on this architecture family: the kernels that read through
+// buffer descriptors (scalar or per-lane offsets, bounds checked against the
+// buffer's size) build theirs with it.
+constexpr int kRawRsrcWord3 = 0x00020000;
+
 // ---------------------------------------------------------------------------
 // Launchers (each returns hipSuccess or the launch error).
 // ---------------------------------------------------------------------------

@@ -19,13 +19,14 @@
 // A work-group computes a 128 x 128 tile of z (patterns x perceptrons) with
 // four waves of 64 x 64.  K is walked in steps of 512 elements (64 bytes of
 // each bit row) through a ring of kStages LDS buffers filled by
-// direct-to-LDS loads (global_load_lds, 16 bytes per lane, or 4 where rows
-// are not 16-byte aligned) three steps ahead of the matrix cores, with one
-// barrier per step; a step's operand words are read from LDS one step
-// ahead, in between the MFMAs.  Rows past the matrix end are clamped into
-// range, and so are loads past the end of a row in the last step: they
-// only feed outputs that are never stored, or elements past K, which are
-// made fp4 zeros in the W_l operand.  The epilogue never writes z to
+// direct-to-LDS buffer loads (16 bytes per lane, or 4 where rows are not
+// 16-byte aligned) three steps ahead of the matrix cores, with one barrier
+// per step; a step's operand words are read from LDS one step ahead, in
+// between the MFMAs.  Rows past the matrix end are clamped into range; a
+// load past the end of a row in the last step reads the next row, or zeros
+// past the matrix (the buffer descriptors are sized to the operands): those
+// bytes only feed outputs that are never stored, or elements past K, which
+// are made fp4 zeros in the W_l operand.  The epilogue never writes z to
 // memory:
 //   * a_l as bit rows (wave ballots);
 //   * for gamma = 64, the easiest wrong perceptron of each group: among the
@@ -65,6 +66,19 @@ __device__ __forceinline__ void dma(const void *src, void *dst_wave_base) {
     __builtin_amdgcn_global_load_lds(src, (lds_void *)dst_wave_base, 16, 0, 0);
   else
     __builtin_amdgcn_global_load_lds(src, (lds_void *)dst_wave_base, 4, 0, 0);
+}
+
+// The same through a buffer descriptor: voff is the lane's byte offset from
+// the buffer's base, which the hardware checks against the buffer's size (a
+// load past the end reads zeros, no fault).  On this architecture family the
+// scalar offset is left out of that check, so every offset goes into voff.
+template <int UNIT>
+__device__ __forceinline__ void bdma(__amdgpu_buffer_rsrc_t rs, uint32_t voff, void *dst_wave_base) {
+  static_assert(UNIT == 16 || UNIT == 4, "load size");
+  if constexpr (UNIT == 16)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)dst_wave_base, 16, voff, 0, 0, 0);
+  else
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)dst_wave_base, 4, voff, 0, 0, 0);
 }
 
 // v_writelane_b32: lane `lane` of the result takes the wave-uniform value
@@ -220,26 +234,33 @@ __global__ __launch_bounds__(256) void fwd_fp4_kernel(const uint64_t *pA, const 
   // of instruction h fills LDS bytes UNIT*l of its kRowsPerDma rows: row
   // r = 32*wave + kRowsPerDma*h + (UNIT*l) / 64, physical 16-byte unit u,
   // which holds logical unit u ^ swz(r) of that row (the XOR swizzle keeps
-  // the operand reads conflict-free).  A source past the end of its row
-  // (only in the last step) is clamped to the row's last UNIT bytes.
-  const uint8_t *srcA[kDma], *srcB[kDma];
-  int offA[kDma];
-  const int rowbytes_a = 8 * S.ld, rowbytes_b = 8 * S.ld;
+  // the operand reads conflict-free).  Rows past the matrix are clamped to
+  // its last row.  A source past the end of its row (only in the last step)
+  // reads the next row's first bytes, elements past K that the last step
+  // masks out, or, past the matrix, zeros: the loads go through buffer
+  // descriptors sized to the matrices, so that a step costs one add per
+  // load and no clamp.
+  uint32_t voffA[kDma], voffB[kDma];
+  const uint32_t rowbytes = 8u * (uint32_t)S.ld;
 #pragma unroll
   for (int h = 0; h < kDma; ++h) {
     const int pos = UNIT * lane;   // byte in the instruction's rows
     const int r = 32 * wave + kRowsPerDma * h + pos / KB;
     const int inrow = pos % KB;
-    offA[h] = 16 * ((inrow / 16) ^ swz(r)) + inrow % 16;
-    srcA[h] = reinterpret_cast<const uint8_t *>(S.A + (size_t)min(m0 + r, pM - 1) * S.ld);
-    srcB[h] = reinterpret_cast<const uint8_t *>(S.B + (size_t)min(n0 + r, pN - 1) * S.ld);
+    const uint32_t off = 16 * ((inrow / 16) ^ swz(r)) + inrow % 16;
+    voffA[h] = (uint32_t)min(m0 + r, pM - 1) * rowbytes + off;
+    voffB[h] = (uint32_t)min(n0 + r, pN - 1) * rowbytes + off;
   }
+  const __amdgpu_buffer_rsrc_t rsA =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint64_t *>(S.A), 0, (int)((uint32_t)pM * rowbytes), kRawRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rsB =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint64_t *>(S.B), 0, (int)((uint32_t)pN * rowbytes), kRawRsrcWord3);
   auto issue = [&](int ks, uint8_t *d) {
+    const uint32_t so = (uint32_t)(ks * KB);
 #pragma unroll
     for (int h = 0; h < kDma; ++h) {
-      const int o = ks * KB + offA[h];
-      dma<UNIT>(srcA[h] + min(o, rowbytes_a - UNIT), d + (kDma * wave + h) * 64 * UNIT);
-      dma<UNIT>(srcB[h] + min(o, rowbytes_b - UNIT), d + TM * KB + (kDma * wave + h) * 64 * UNIT);
+      bdma<UNIT>(rsA, voffA[h] + so, d + (kDma * wave + h) * 64 * UNIT);
+      bdma<UNIT>(rsB, voffB[h] + so, d + TM * KB + (kDma * wave + h) * 64 * UNIT);
     }
   };
 

@@ -144,10 +144,7 @@ __device__ __forceinline__ void add_count(uint32_t (&c)[kPlanes], const uint32_t
 
 // The a_{l-1} rows are read through a buffer descriptor: the selector's row
 // offset is a scalar (soffset) and the lane's word offset a vector register,
-// so a load costs no vector address arithmetic.  kRawRsrcWord3 is the fourth
-// descriptor word of a raw (stride 0) buffer of 32-bit words on this
-// architecture family.
-constexpr int kRawRsrcWord3 = 0x00020000;
+// so a load costs no vector address arithmetic.
 
 __device__ __forceinline__ uint32_t load_word(__amdgpu_buffer_rsrc_t rs, int voff, int soff) {
   return __builtin_amdgcn_raw_buffer_load_b32(rs, voff, soff, 0);
