@@ -651,6 +651,9 @@ hipError_t launch_fwd_fp4(FwdArgs &a, hipStream_t s) {
     // and the stride is an even number of words
     aligned = aligned && q.ld % 2 == 0 && (reinterpret_cast<uintptr_t>(q.A) & 15) == 0 &&
               (reinterpret_cast<uintptr_t>(q.B) & 15) == 0;
+    // the kernel's buffer descriptors hold each operand's size in bytes as a
+    // 32-bit signed count
+    if ((int64_t)a.M * q.ld * 8 > INT32_MAX || (int64_t)a.N * q.ld * 8 > INT32_MAX) return hipErrorInvalidValue;
     bytes_a += (double)a.M * q.ld;
     bytes_b += (double)a.N * q.ld;
   }
